@@ -1,0 +1,196 @@
+/*
+ * pp_attn.h -- C ABI of the preference-packing hot path for AMD MI355X (gfx950).
+ *
+ * Preference packing (Sec. 3.2 of "Preference Packing: Efficient Preference
+ * Optimization for Large Language Models") writes one prompt once and then its
+ * K ranked responses one after another in a single row; a causal mask lets every
+ * response see the whole prompt and its own earlier tokens but never another
+ * response, and position IDs keep each token's unpacked position.  The library
+ * computes, on one GPU:
+ *
+ *   pp_attn_fwd     masked attention forward over packed rows  (Sec. 3.2)
+ *   pp_attn_bwd     its gradients dQ, dK, dV                   (Sec. 3.2)
+ *   pp_seq_logprob  per-response summed token log-probs        (Sec. 2.1, Sec. 3.2)
+ *   pp_dpo_loss     ranked-pair DPO / Bradley-Terry loss        (Sec. 2.1)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  Every pointer named "dev" is device memory owned by the caller;
+ *   every pointer named "host" is host memory read before the call returns.
+ *   The library allocates no device memory; it keeps a small ring of pinned host
+ *   staging buffers for plan metadata, freed when the library is unloaded.
+ * Streams.  All device work is enqueued on `hip_stream` (a hipStream_t; NULL
+ *   means the null stream) in call order; no entry point synchronises the device.
+ * Errors.  Arguments are validated on the host before anything is enqueued; a
+ *   failed validation returns an error code and enqueues nothing.  A HIP error
+ *   while enqueuing returns PP_ERR_HIP.  No entry point throws or aborts.
+ *   pp_last_error() returns a human-readable message for the last failure on the
+ *   calling thread.
+ * Concurrency.  Calls may be made from several host threads; calls that share a
+ *   workspace must be ordered on one stream.
+ *
+ * The packed layout (pp_pack_desc)
+ * --------------------------------
+ * B rows are concatenated on one flat token axis of sumT = row_start[B] tokens.
+ * Row b spans [row_start[b], row_start[b+1]) (its capacity T_b).  Its prompt is
+ * the first P_b = prompt_len[b] tokens; response k (0 <= k < K_b = num_resp[b])
+ * is [resp_off[b*max_resp+k], + resp_len[b*max_resp+k]) relative to the row
+ * start.  Responses are contiguous: resp_off[b,0] = P_b and resp_off[b,k+1] =
+ * resp_off[b,k] + resp_len[b,k] ("sequentially pack", Sec. 1 and Sec. 3.2), and
+ * P_b + sum_k resp_len[b,k] <= T_b.  Tokens after that are padding: their
+ * attention output, LSE and gradients are written as 0.  Responses are in the
+ * paper's ranking order: a larger index is preferred (Sec. 3.1).
+ *
+ * Mask (Sec. 3.2; Figure 1 is described only by its caption): query i sees key
+ * j iff j <= i, neither is padding, and j is a prompt token or lies in the same
+ * response as i.  q-head h reads kv-head h / (hq / hkv).
+ *
+ * Tensor layouts (row-major, contiguous):
+ *   q, o, dout, dq      [sumT, hq,  head_dim]
+ *   k, v, dk, dv        [sumT, hkv, head_dim]
+ *   lse                 [hq, sumT] float, natural log of the softmax denominator
+ *   logits              [sumT, vocab]: row t holds the next-token logits produced
+ *                       at packed position t
+ *   tokens              [sumT] int32 packed input ids
+ */
+#ifndef PP_ATTN_H
+#define PP_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pp_status {
+  PP_OK = 0,
+  PP_ERR_INVALID_ARGUMENT = 1,  /* null pointer, bad count or size, no loss pair */
+  PP_ERR_BAD_LAYOUT = 2,        /* descriptor violates the packed layout above */
+  PP_ERR_UNSUPPORTED = 3,       /* valid but not implemented (e.g. head_dim)  */
+  PP_ERR_WORKSPACE_TOO_SMALL = 4,
+  PP_ERR_HIP = 5                /* a HIP runtime call failed */
+} pp_status;
+
+typedef enum pp_dtype {
+  PP_BF16 = 0,  /* bfloat16 */
+  PP_FP32 = 1   /* float; attention rounds it to bf16 (nearest even) at tile load */
+} pp_dtype;
+
+/* Host description of a packed batch; see "The packed layout" above. */
+typedef struct pp_pack_desc {
+  int32_t num_rows;          /* B >= 1 */
+  int32_t max_resp;          /* K_max >= 0: stride of resp_off / resp_len */
+  const int32_t* row_start;  /* host [B+1], row_start[0] = 0, non-decreasing */
+  const int32_t* prompt_len; /* host [B], P_b >= 0 */
+  const int32_t* num_resp;   /* host [B], 0 <= K_b <= K_max */
+  const int32_t* resp_off;   /* host [B*K_max], row-relative */
+  const int32_t* resp_len;   /* host [B*K_max], >= 0 */
+} pp_pack_desc;
+
+/* Device workspace (bytes) that each entry point needs for this batch.
+ * Any output pointer may be NULL.  vocab is used only for logprob and may be 0.
+ * hq, hkv and head_dim are validated as for pp_attn_fwd when fwd or bwd is
+ * requested.  loss is the workspace of pp_dpo_loss for this batch's B. */
+pp_status pp_workspace_size(const pp_pack_desc* desc, int hq, int hkv, int head_dim, int vocab,
+                            size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss);
+
+/* Forward packed attention (Sec. 3.2): for every non-padding query i and head h
+ *   O[i,h]   = sum_j softmax_j(scale * q[i,h] . k[j,g]) v[j,g] over the keys j
+ *              that query i sees, g = h / (hq/hkv);
+ *   lse[h,i] = ln sum_j exp(scale * q[i,h] . k[j,g]).
+ * Padding queries get O = 0 and lse = 0.
+ * dtype: PP_BF16 or PP_FP32 for q, k, v and o (fp32 is rounded to bf16 on load;
+ * products accumulate in fp32).  head_dim in {64, 128}; hq % hkv == 0.
+ * scale <= 0 selects 1/sqrt(head_dim).
+ * Errors: PP_ERR_UNSUPPORTED for another head_dim; PP_ERR_INVALID_ARGUMENT for
+ * null pointers or bad head counts; PP_ERR_BAD_LAYOUT for a bad descriptor;
+ * PP_ERR_WORKSPACE_TOO_SMALL if ws_bytes is below pp_workspace_size's fwd. */
+pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      float scale, const void* q, const void* k, const void* v, void* o,
+                      float* lse, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Backward of pp_attn_fwd: gradients of sum(dout * O) (Sec. 3.2).
+ *   dV[j,g] = sum_{h in g} sum_i P_ij dO[i,h]
+ *   dS_ij   = P_ij (dO[i,h] . v[j,g] - dO[i,h] . O[i,h])
+ *   dQ[i,h] = scale sum_j dS_ij k[j,g]
+ *   dK[j,g] = scale sum_{h in g} sum_i dS_ij q[i,h]
+ * The gradient of a prompt key gathers the contributions of the prompt's own
+ * queries and of every response's queries (the prompt is stored once).
+ * o and lse are the outputs of pp_attn_fwd on the same inputs.  dq, dk, dv have
+ * the input dtype; padding rows are written as 0.  The result is deterministic
+ * (no atomics).  Errors as pp_attn_fwd; ws_bytes >= pp_workspace_size's bwd. */
+pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      float scale, const void* q, const void* k, const void* v, const void* o,
+                      const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
+                      size_t ws_bytes, void* hip_stream);
+
+/* Per-response sequence log-probabilities (Sec. 2.1 scores, Sec. 3.2 layout).
+ * Token j of response k of row b sits at row-relative position t = o_bk + j; it
+ * is predicted by the logits at position P_b - 1 when j = 0 (the last prompt
+ * token, shared by all K responses) and at t - 1 otherwise, with label
+ * tokens[t].  Its log-prob is logit[label] - ln sum_v exp(logit[v]), computed in
+ * fp32.  seq_logp[b*K_max+k] (dev, float) = sum over the response's tokens, in
+ * token order; empty responses and slots k >= K_b get 0.  tok_logp (dev, float
+ * [sumT], may be NULL) receives each response token's log-prob at its own
+ * position and 0 at every other position.  A label outside [0, vocab) makes that
+ * response's sum NaN.  Only the logit rows that predict a response token are
+ * read.  logits_dtype: PP_BF16 or PP_FP32.
+ * Errors: PP_ERR_BAD_LAYOUT also when a row has P_b = 0 and a non-empty response
+ * (its first token has no predicting position). */
+pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                         const void* logits, const int32_t* tokens, float* seq_logp,
+                         float* tok_logp, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Ranked-pair DPO / Bradley-Terry loss (Sec. 2.1, extended to K > 2).
+ * z_k = beta (logp_pol[b,k] - logp_ref[b,k]), or beta logp_pol[b,k] when
+ * logp_ref is NULL (reward-model scores).  For every pair a > c of row b's first
+ * K_b slots (slot a preferred, Sec. 3.1) the term is softplus(-(z_a - z_c)) =
+ * -ln sigmoid(z_a - z_c).  row_loss[b] = mean over the row's K_b(K_b-1)/2 pairs
+ * (0 for rows with K_b < 2); *loss = mean of row_loss over rows with K_b >= 2;
+ * dlogp_pol[b,k] = d(*loss)/d(logp_pol[b,k]).
+ * num_resp is host [B]; logp_pol, logp_ref, loss, row_loss, dlogp_pol are dev
+ * float; row_loss and dlogp_pol may be NULL.  ws_bytes >= pp_workspace_size's
+ * loss.  PP_ERR_INVALID_ARGUMENT when no row has two responses. */
+pp_status pp_dpo_loss(int32_t num_rows, int32_t max_resp, const int32_t* num_resp,
+                      const float* logp_pol, const float* logp_ref, float beta, float* loss,
+                      float* row_loss, float* dlogp_pol, void* ws, size_t ws_bytes,
+                      void* hip_stream);
+
+/* Host-only export of the planner's integer view of a batch (no GPU needed):
+ *   position_ids[sumT]  prompt token t -> t, response token j -> P_b + j,
+ *                       padding -> 0 (Sec. 3.2: original positions kept);
+ *   segment_ids[sumT]   0 prompt, k+1 response k, -1 padding;
+ *   tile_class          for every row, its ceil(T_b/block_q) x ceil(T_b/block_k)
+ *                       grid of mask tiles, row-major, rows concatenated:
+ *                       0 EMPTY (no visible pair), 1 PARTIAL, 2 FULL (every pair
+ *                       of the tile, clipped to the row, visible).
+ * Any output may be NULL.  tile_class_len must be at least the total grid size
+ * when tile_class is not NULL (PP_ERR_INVALID_ARGUMENT otherwise). */
+pp_status pp_pack_export(const pp_pack_desc* desc, int block_q, int block_k, int32_t* position_ids,
+                         int32_t* segment_ids, uint8_t* tile_class, size_t tile_class_len);
+
+/* Number of tile_class entries pp_pack_export writes for (block_q, block_k). */
+pp_status pp_tile_class_len(const pp_pack_desc* desc, int block_q, int block_k, size_t* len);
+
+/* Kernel timing for measurement.  While enabled, each kernel launch of this
+ * library is bracketed by two hipEvents recorded on its own stream.
+ * pp_timing_count returns how many distinct kernels were timed since the last
+ * reset; pp_timing_get waits for their events and returns, for entry idx, the
+ * kernel's name (static string), its total elapsed milliseconds and its launch
+ * count. */
+pp_status pp_timing_enable(int on);
+pp_status pp_timing_reset(void);
+int pp_timing_count(void);
+pp_status pp_timing_get(int idx, const char** name, double* total_ms, int64_t* launches);
+
+const char* pp_status_string(pp_status status);
+const char* pp_last_error(void);
+/* ABI version: major * 10000 + minor * 100 + patch. */
+int pp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PP_ATTN_H */

@@ -1,0 +1,265 @@
+"""Thin ctypes binding of libppattn.so (include/pp_attn.h).
+
+Each function has the name of the C entry point it calls and only marshals
+arguments: it takes torch tensors for device memory, passes their data pointers
+and the current HIP stream, allocates outputs and the workspace with torch, and
+raises PPError on a non-zero status.  Every step of the computation runs in the
+library's HIP kernels; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+from .workload import Pack
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libppattn.so")
+
+PP_OK = 0
+PP_BF16 = 0
+PP_FP32 = 1
+STATUS = {0: "PP_OK", 1: "PP_ERR_INVALID_ARGUMENT", 2: "PP_ERR_BAD_LAYOUT", 3: "PP_ERR_UNSUPPORTED",
+          4: "PP_ERR_WORKSPACE_TOO_SMALL", 5: "PP_ERR_HIP"}
+
+EXPORTED = [
+    "pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_dpo_loss",
+    "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
+    "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
+]
+
+
+class PPError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [
+        ("num_rows", ctypes.c_int32),
+        ("max_resp", ctypes.c_int32),
+        ("row_start", ctypes.POINTER(ctypes.c_int32)),
+        ("prompt_len", ctypes.POINTER(ctypes.c_int32)),
+        ("num_resp", ctypes.POINTER(ctypes.c_int32)),
+        ("resp_off", ctypes.POINTER(ctypes.c_int32)),
+        ("resp_len", ctypes.POINTER(ctypes.c_int32)),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads the built library (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_24082_amd.build` "
+                          "(there is no non-HIP fallback)")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    i32 = ctypes.c_int32
+    i = ctypes.c_int
+    sz = ctypes.c_size_t
+    D = ctypes.POINTER(_Desc)
+    L.pp_workspace_size.argtypes = [D, i, i, i, i, ctypes.POINTER(sz), ctypes.POINTER(sz),
+                                    ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    L.pp_attn_fwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, sz, P]
+    L.pp_attn_bwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, P, P, P, P, sz, P]
+    L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
+    L.pp_dpo_loss.argtypes = [i32, i32, P, P, P, ctypes.c_float, P, P, P, P, sz, P]
+    L.pp_pack_export.argtypes = [D, i, i, P, P, P, sz]
+    L.pp_tile_class_len.argtypes = [D, i, i, ctypes.POINTER(sz)]
+    L.pp_timing_enable.argtypes = [i]
+    L.pp_timing_reset.argtypes = []
+    L.pp_timing_count.argtypes = []
+    L.pp_timing_count.restype = i
+    L.pp_timing_get.argtypes = [i, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
+                                ctypes.POINTER(ctypes.c_int64)]
+    L.pp_status_string.argtypes = [i]
+    L.pp_status_string.restype = ctypes.c_char_p
+    L.pp_last_error.argtypes = []
+    L.pp_last_error.restype = ctypes.c_char_p
+    L.pp_version.restype = i
+    for name in ("pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_dpo_loss",
+                 "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
+                 "pp_timing_get"):
+        getattr(L, name).restype = i
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != PP_OK:
+        raise PPError(status, lib().pp_last_error().decode())
+
+
+class _DescHolder:
+    """Keeps the int32 arrays of a Pack alive while the C struct points at them."""
+
+    def __init__(self, pack: Pack):
+        c = lambda a: np.ascontiguousarray(a, dtype=np.int32)
+        self.arrays = [c(pack.row_start), c(pack.prompt_len), c(pack.num_resp),
+                       c(pack.resp_off).reshape(-1), c(pack.resp_len).reshape(-1)]
+        ptr = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        self.desc = _Desc(pack.num_rows, pack.max_resp, *[ptr(a) for a in self.arrays])
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.desc)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PP_BF16
+    if t.dtype == torch.float32:
+        return PP_FP32
+    raise TypeError(f"unsupported dtype {t.dtype} (bf16 or fp32)")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def pp_workspace_size(pack: Pack, hq: int = 1, hkv: int = 1, head_dim: int = 64, vocab: int = 0,
+                      fwd=True, bwd=True, logprob=False, loss=True):
+    """Workspace bytes (fwd, bwd, logprob, loss); entries not asked for are None."""
+    h = _DescHolder(pack)
+    vals = [ctypes.c_size_t(0) for _ in range(4)]
+    want = [fwd, bwd, logprob, loss]
+    args = [ctypes.byref(v) if w else None for v, w in zip(vals, want)]
+    _check(lib().pp_workspace_size(h.ref, hq, hkv, head_dim, vocab, *args))
+    return tuple(int(v.value) if w else None for v, w in zip(vals, want))
+
+
+def pp_attn_fwd(pack: Pack, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float = 0.0,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                ws: Optional[torch.Tensor] = None):
+    """Packed attention forward; returns (o [sumT,hq,d], lse [hq,sumT] fp32)."""
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    h = _DescHolder(pack)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty(hq, T, dtype=torch.float32, device=q.device)
+    if ws is None:
+        nb, = pp_workspace_size(pack, hq, hkv, d, fwd=True, bwd=False, loss=False)[:1]
+        ws = _workspace(nb, q.device)
+    _check(lib().pp_attn_fwd(h.ref, _dtype_code(q), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v),
+                             _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(q.device)))
+    return out, lse
+
+
+def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, dk=None, dv=None,
+                ws=None):
+    """Packed attention backward; returns (dq, dk, dv) in the input dtype."""
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    h = _DescHolder(pack)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    if ws is None:
+        nb = pp_workspace_size(pack, hq, hkv, d, fwd=False, bwd=True, loss=False)[1]
+        ws = _workspace(nb, q.device)
+    _check(lib().pp_attn_bwd(h.ref, _dtype_code(q), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v),
+                             _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),
+                             ws.numel(), _stream(q.device)))
+    return dq, dk, dv
+
+
+def pp_seq_logprob(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, want_tok: bool = False,
+                   seq=None, tok=None, ws=None):
+    """Per-response summed log-probs [B, K_max] (and per-token [sumT] if asked)."""
+    V = logits.shape[1]
+    h = _DescHolder(pack)
+    dev = logits.device
+    if seq is None:
+        seq = torch.empty(pack.num_rows, max(pack.max_resp, 1), dtype=torch.float32, device=dev)
+    if want_tok and tok is None:
+        tok = torch.empty(logits.shape[0], dtype=torch.float32, device=dev)
+    if ws is None:
+        nb = pp_workspace_size(pack, vocab=V, fwd=False, bwd=False, logprob=True, loss=False)[2]
+        ws = _workspace(nb, dev)
+    if tokens.dtype != torch.int32:
+        raise TypeError("tokens must be int32")
+    _check(lib().pp_seq_logprob(h.ref, _dtype_code(logits), V, _ptr(logits), _ptr(tokens), _ptr(seq),
+                                _ptr(tok), _ptr(ws), ws.numel(), _stream(dev)))
+    return (seq, tok) if want_tok else seq
+
+
+def pp_dpo_loss(num_resp, logp_pol: torch.Tensor, logp_ref: Optional[torch.Tensor], beta: float,
+                want_rows: bool = True, want_grad: bool = True, ws=None):
+    """Ranked-pair DPO / BT loss; returns (loss [1], row_loss [B] or None, dlogp [B,K] or None)."""
+    nr = np.ascontiguousarray(num_resp, dtype=np.int32)
+    B, K = logp_pol.shape
+    dev = logp_pol.device
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    rows = torch.empty(B, dtype=torch.float32, device=dev) if want_rows else None
+    grad = torch.empty(B, K, dtype=torch.float32, device=dev) if want_grad else None
+    if ws is None:
+        ws = _workspace((B * 4 + 255) // 256 * 256, dev)
+    _check(lib().pp_dpo_loss(B, K, ctypes.c_void_p(nr.ctypes.data), _ptr(logp_pol), _ptr(logp_ref),
+                             float(beta), _ptr(loss), _ptr(rows), _ptr(grad), _ptr(ws), ws.numel(),
+                             _stream(dev)))
+    return loss, rows, grad
+
+
+def pp_pack_export(pack: Pack, block_q: int = 128, block_k: int = 64, tiles: bool = True):
+    """Host-only integer export: (position_ids, segment_ids, tile_class) numpy arrays."""
+    h = _DescHolder(pack)
+    T = pack.total_tokens
+    pos = np.zeros(T, np.int32)
+    seg = np.zeros(T, np.int32)
+    n = ctypes.c_size_t(0)
+    tc = None
+    if tiles:
+        _check(lib().pp_tile_class_len(h.ref, block_q, block_k, ctypes.byref(n)))
+        tc = np.zeros(n.value, np.uint8)
+    _check(lib().pp_pack_export(h.ref, block_q, block_k, ctypes.c_void_p(pos.ctypes.data),
+                                ctypes.c_void_p(seg.ctypes.data),
+                                ctypes.c_void_p(tc.ctypes.data) if tiles else None, n.value))
+    return pos, seg, tc
+
+
+# ---------------------------------------------------------------- timing
+
+
+def pp_timing_enable(on: bool = True):
+    _check(lib().pp_timing_enable(1 if on else 0))
+
+
+def pp_timing_reset():
+    _check(lib().pp_timing_reset())
+
+
+def pp_timing_get() -> dict:
+    """{kernel name: (total ms, launches)} since the last reset (waits for events)."""
+    L = lib()
+    out = {}
+    for idx in range(L.pp_timing_count()):
+        name = ctypes.c_char_p()
+        ms = ctypes.c_double()
+        n = ctypes.c_int64()
+        _check(L.pp_timing_get(idx, ctypes.byref(name), ctypes.byref(ms), ctypes.byref(n)))
+        out[name.value.decode()] = (ms.value, n.value)
+    return out

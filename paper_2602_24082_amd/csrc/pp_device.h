@@ -1,0 +1,117 @@
+// Device helpers for the gfx950 (CDNA4) kernels: bf16 vector types, loads that
+// round fp32 inputs to bf16, the 32x32x16 bf16 MFMA and its register layout.
+//
+// v_mfma_f32_32x32x16_bf16 (wave64) computes D[32x32] += A[32x16] * B[16x32]:
+//   A operand: lane l holds A[m = l%32][k = 8*(l/32) + e], e = 0..7
+//   B operand: lane l holds B[k = 8*(l/32) + e][n = l%32], e = 0..7
+//   D/C:       lane l holds D[m = 8*(r/4) + 4*(l/32) + r%4][n = l%32], r = 0..15
+// Both operands therefore read 8 consecutive elements along the contraction
+// axis, and the result's column n is owned by lanes l and l+32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
+
+// 8 consecutive elements as bf16 (fp32 input is rounded to nearest even).
+template <typename T>
+__device__ __forceinline__ bf16x8 load8_bf16(const T* p);
+
+template <>
+__device__ __forceinline__ bf16x8 load8_bf16<__bf16>(const __bf16* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+
+template <>
+__device__ __forceinline__ bf16x8 load8_bf16<float>(const float* p) {
+  const f32x4 a = *reinterpret_cast<const f32x4*>(p);
+  const f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+  f32x8 x = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_convertvector(x, bf16x8);
+}
+
+// Stores 4 consecutive outputs in the tensor's element type.
+template <typename T>
+__device__ __forceinline__ void store4(T* p, f32x4 v);
+
+template <>
+__device__ __forceinline__ void store4<__bf16>(__bf16* p, f32x4 v) {
+  *reinterpret_cast<bf16x4*>(p) = __builtin_convertvector(v, bf16x4);
+}
+
+template <>
+__device__ __forceinline__ void store4<float>(float* p, f32x4 v) {
+  *reinterpret_cast<f32x4*>(p) = v;
+}
+
+__device__ __forceinline__ bf16x8 to_bf16x8(float a0, float a1, float a2, float a3, float a4, float a5,
+                                             float a6, float a7) {
+  f32x8 x = {a0, a1, a2, a3, a4, a5, a6, a7};
+  return __builtin_convertvector(x, bf16x8);
+}
+
+// The 16 accumulator registers r = 8s..8s+7 (s = 0, 1) of a 32x32 result, as a
+// bf16 B operand of a K=16 MFMA.  Lane half h = l/32 then holds rows
+// 16s + 8*(e/4) + 4h + e%4 for e = 0..7, i.e. the contraction index
+// kk = 8h + e stands for row 16s + perm16(kk) with
+//   perm16(kk) = 8*((kk%8)/4) + 4*(kk/8) + kk%4.
+// An A operand read from LDS must use the same order, which the kernels get by
+// storing groups of four rows at position kRowGroupPos[group] inside each
+// 16-row chunk: rows 0-3 -> 0, 4-7 -> 8, 8-11 -> 4, 12-15 -> 12.
+__device__ __forceinline__ bf16x8 acc_half_to_bf16(const f32x16& acc, int s) {
+  return to_bf16x8(acc[8 * s + 0], acc[8 * s + 1], acc[8 * s + 2], acc[8 * s + 3], acc[8 * s + 4],
+                   acc[8 * s + 5], acc[8 * s + 6], acc[8 * s + 7]);
+}
+
+__device__ __forceinline__ int row_group_pos(int group) {
+  // position of the 4-row group `group` inside its 16-row chunk, plus the chunk base
+  const int g = group & 3;
+  const int p = (g == 0) ? 0 : (g == 1) ? 8 : (g == 2) ? 4 : 12;
+  return (group >> 2) * 16 + p;
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+  for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
+// Maps a linear workgroup index to (item, head).  Workgroups are dispatched to
+// the 8 XCDs round-robin (index % 8); when the head count is a multiple of 8 the
+// heads of one item are arranged so that each XCD receives a contiguous run of
+// heads, which for grouped-query attention is one kv-head's query group, so its
+// K/V tiles are shared through that XCD's L2.
+__device__ __forceinline__ void item_and_head(int block, int heads, int& item, int& head) {
+  item = block / heads;
+  const int r = block - item * heads;
+  if ((heads & 7) == 0) {
+    const int per = heads >> 3;
+    head = (r & 7) * per + (r >> 3);
+  } else {
+    head = r;
+  }
+}
+
+}  // namespace pp

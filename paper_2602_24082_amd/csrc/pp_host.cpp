@@ -1,0 +1,869 @@
+// Host side of the preference-packing library: descriptor validation, the
+// planner that turns a packed batch (Sec. 3.2) into tile work lists, workspace
+// layout, pinned staging of plan metadata, kernel timing and the C ABI entry
+// points declared in pp_attn.h.
+//
+// Validation never touches the GPU, so every error path (and pp_pack_export)
+// works on a machine without one.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/pp_attn.h"
+#include "pp_launch.h"
+#include "pp_plan.h"
+
+namespace pp {
+namespace {
+
+thread_local std::string g_last_error;
+
+pp_status fail(pp_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+pp_status hip_fail(hipError_t e, const char* what) {
+  return fail(PP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// Descriptor validation and per-row view
+// ---------------------------------------------------------------------------
+
+struct Row {
+  int32_t tok0;  // flat start
+  int32_t T;     // capacity
+  int32_t P;     // prompt length
+  int32_t K;     // responses
+  int32_t valid; // P + sum L
+  const int32_t* off;
+  const int32_t* len;
+};
+
+struct Batch {
+  std::vector<Row> rows;
+  int32_t sumT = 0;
+  int32_t B = 0;
+  int32_t Kmax = 0;
+};
+
+pp_status read_desc(const pp_pack_desc* d, Batch* out) {
+  if (!d) return fail(PP_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->num_rows < 1) return fail(PP_ERR_INVALID_ARGUMENT, "num_rows must be >= 1 (got %d)", d->num_rows);
+  if (d->max_resp < 0) return fail(PP_ERR_INVALID_ARGUMENT, "max_resp must be >= 0");
+  if (!d->row_start || !d->prompt_len || !d->num_resp)
+    return fail(PP_ERR_INVALID_ARGUMENT, "row_start, prompt_len and num_resp must be non-NULL");
+  if (d->max_resp > 0 && (!d->resp_off || !d->resp_len))
+    return fail(PP_ERR_INVALID_ARGUMENT, "resp_off and resp_len must be non-NULL when max_resp > 0");
+  const int B = d->num_rows;
+  if (d->row_start[0] != 0) return fail(PP_ERR_BAD_LAYOUT, "row_start[0] must be 0");
+  out->rows.resize(B);
+  out->B = B;
+  out->Kmax = d->max_resp;
+  for (int b = 0; b < B; ++b) {
+    const int64_t r0 = d->row_start[b], r1 = d->row_start[b + 1];
+    if (r1 < r0) return fail(PP_ERR_BAD_LAYOUT, "row_start must be non-decreasing (row %d)", b);
+    Row& r = out->rows[b];
+    r.tok0 = (int32_t)r0;
+    r.T = (int32_t)(r1 - r0);
+    r.P = d->prompt_len[b];
+    r.K = d->num_resp[b];
+    if (r.P < 0) return fail(PP_ERR_BAD_LAYOUT, "prompt_len[%d] < 0", b);
+    if (r.K < 0 || r.K > d->max_resp)
+      return fail(PP_ERR_BAD_LAYOUT, "num_resp[%d] = %d outside [0, max_resp=%d]", b, r.K, d->max_resp);
+    r.off = d->max_resp ? d->resp_off + (int64_t)b * d->max_resp : nullptr;
+    r.len = d->max_resp ? d->resp_len + (int64_t)b * d->max_resp : nullptr;
+    int64_t pos = r.P;
+    for (int k = 0; k < r.K; ++k) {
+      if (r.len[k] < 0) return fail(PP_ERR_BAD_LAYOUT, "resp_len[%d,%d] < 0", b, k);
+      if (r.off[k] != pos)
+        return fail(PP_ERR_BAD_LAYOUT,
+                    "responses must follow the prompt contiguously: resp_off[%d,%d] = %d, expected %lld",
+                    b, k, r.off[k], (long long)pos);
+      pos += r.len[k];
+    }
+    if (pos > r.T)
+      return fail(PP_ERR_BAD_LAYOUT, "row %d: prompt + responses = %lld exceed its %d tokens", b,
+                  (long long)pos, r.T);
+    r.valid = (int32_t)pos;
+  }
+  out->sumT = d->row_start[B];
+  return PP_OK;
+}
+
+pp_status check_heads(int hq, int hkv, int d) {
+  if (hq < 1 || hkv < 1) return fail(PP_ERR_INVALID_ARGUMENT, "hq and hkv must be >= 1");
+  if (hq % hkv) return fail(PP_ERR_INVALID_ARGUMENT, "hq (%d) must be a multiple of hkv (%d)", hq, hkv);
+  if (d != 64 && d != 128) return fail(PP_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", d);
+  return PP_OK;
+}
+
+pp_status check_dtype(pp_dtype t) {
+  if (t != PP_BF16 && t != PP_FP32) return fail(PP_ERR_INVALID_ARGUMENT, "unknown dtype %d", (int)t);
+  return PP_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Exact visible-pair counting on intervals
+// ---------------------------------------------------------------------------
+
+inline int64_t overlap(int64_t a0, int64_t a1, int64_t b0, int64_t b1) {
+  const int64_t lo = std::max(a0, b0), hi = std::min(a1, b1);
+  return hi > lo ? hi - lo : 0;
+}
+
+// Row-relative start of the segment holding token t (0 for the prompt), or -1
+// for padding.
+inline int32_t seg_start(const Row& r, int32_t t) {
+  if (t < r.P) return 0;
+  if (t >= r.valid) return -1;
+  // responses are contiguous from P, so the last offset <= t wins
+  int32_t lo = r.P;
+  for (int k = 0; k < r.K; ++k) {
+    if (r.off[k] <= t && t < r.off[k] + r.len[k]) return r.off[k];
+    if (r.off[k] <= t) lo = r.off[k];
+  }
+  return lo;
+}
+
+// Segment id: 0 prompt, k+1 response k, -1 padding.
+inline int32_t seg_id(const Row& r, int32_t t) {
+  if (t < r.P) return 0;
+  for (int k = 0; k < r.K; ++k)
+    if (r.off[k] <= t && t < r.off[k] + r.len[k]) return k + 1;
+  return -1;
+}
+
+// sum_{i=a}^{b-1} max(0, min(k1, i+1) - c): the keys in [c, k1) that lie at or
+// before query i, summed over a run of queries.
+int64_t sum_ramp(int64_t a, int64_t b, int64_t c, int64_t k1) {
+  if (b <= a || k1 <= c) return 0;
+  int64_t n = 0;
+  // x = i + 1 runs over [a+1, b]; x in (c, k1] contributes x - c
+  const int64_t lo1 = std::max(a + 1, c + 1), hi1 = std::min(b, k1);
+  if (hi1 >= lo1) n += (lo1 - c + hi1 - c) * (hi1 - lo1 + 1) / 2;
+  // x in (k1, b] contributes k1 - c
+  const int64_t lo2 = std::max(a + 1, k1 + 1);
+  if (b >= lo2) n += (b - lo2 + 1) * (k1 - c);
+  return n;
+}
+
+// Number of visible (query, key) pairs with query in [q0,q1), key in [k0,k1),
+// in closed form per segment.  A prompt query i sees keys [0, i]; a query i of
+// response k sees [0, P) and [o_k, i]; padding sees nothing.
+int64_t visible_pairs(const Row& r, int32_t q0, int32_t q1, int32_t k0, int32_t k1) {
+  if (k1 <= k0) return 0;
+  int64_t n = 0;
+  // prompt queries
+  {
+    const int64_t a = q0, b = std::min(q1, r.P);
+    n += sum_ramp(a, b, k0, k1);
+  }
+  // response queries
+  const int64_t kp = overlap(k0, k1, 0, r.P);
+  for (int k = 0; k < r.K; ++k) {
+    const int64_t o = r.off[k], e = (int64_t)r.off[k] + r.len[k];
+    const int64_t a = std::max<int64_t>(q0, o), b = std::min<int64_t>(q1, e);
+    if (b <= a) continue;
+    n += kp * (b - a) + sum_ramp(a, b, std::max<int64_t>(k0, o), k1);
+  }
+  return n;
+}
+
+// 0 EMPTY, 1 PARTIAL, 2 FULL for the tile clipped to the row.
+uint8_t classify_tile(const Row& r, int32_t q0, int32_t q1, int32_t k0, int32_t k1) {
+  const int64_t n = visible_pairs(r, q0, q1, k0, k1);
+  if (n == 0) return 0;
+  if (n == (int64_t)(q1 - q0) * (k1 - k0)) return 2;
+  return 1;
+}
+
+// ---------------------------------------------------------------------------
+// Plans
+// ---------------------------------------------------------------------------
+
+struct QPlan {
+  std::vector<QTileItem> items;
+  std::vector<int32_t> ktiles;
+};
+
+void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
+  out->items.clear();
+  out->ktiles.clear();
+  for (int b = 0; b < bt.B; ++b) {
+    const Row& r = bt.rows[b];
+    for (int32_t q0 = 0; q0 < r.T; q0 += BM) {
+      QTileItem it{};
+      it.tok0 = r.tok0;
+      it.q0 = q0;
+      it.q_end = std::min(r.T, q0 + BM);
+      it.P = r.P;
+      it.valid = r.valid;
+      it.kt_off = (int32_t)out->ktiles.size();
+      it.row = b;
+      // only keys <= the tile's last query can be visible (causal)
+      const int32_t kmax = std::min(it.q_end, r.valid);
+      for (int32_t k0 = 0; k0 < kmax; k0 += BN) {
+        const int32_t k1 = std::min(r.T, k0 + BN);
+        if (visible_pairs(r, q0, it.q_end, k0, k1) > 0) out->ktiles.push_back(k0);
+      }
+      it.kt_cnt = (int32_t)out->ktiles.size() - it.kt_off;
+      out->items.push_back(it);
+    }
+  }
+  // longest-first, so the heaviest tiles start in the first wave of workgroups
+  std::stable_sort(out->items.begin(), out->items.end(),
+                   [](const QTileItem& a, const QTileItem& b) { return a.kt_cnt > b.kt_cnt; });
+}
+
+void build_kplan(const Batch& bt, int BN, std::vector<KTileItem>* out) {
+  out->clear();
+  for (int b = 0; b < bt.B; ++b) {
+    const Row& r = bt.rows[b];
+    for (int32_t k0 = 0; k0 < r.T; k0 += BN) {
+      KTileItem it{};
+      it.tok0 = r.tok0;
+      it.k0 = k0;
+      it.k_end = std::min(r.T, k0 + BN);
+      it.P = r.P;
+      it.valid = r.valid;
+      it.row = b;
+      if (k0 >= r.valid) {
+        it.q_begin = it.q_end = k0;  // padding keys: nothing sees them
+      } else {
+        it.q_begin = k0;  // query k0 sees key k0
+        if (k0 < r.P) {
+          it.q_end = r.valid;  // a prompt key is seen by every later real token
+        } else {
+          // keys lie in responses; the last real key's response bounds the range
+          const int32_t last = std::min(it.k_end, r.valid) - 1;
+          int32_t end = r.valid;
+          for (int k = 0; k < r.K; ++k)
+            if (r.off[k] <= last && last < r.off[k] + r.len[k]) end = r.off[k] + r.len[k];
+          it.q_end = end;
+        }
+      }
+      out->push_back(it);
+    }
+  }
+  std::stable_sort(out->begin(), out->end(), [](const KTileItem& a, const KTileItem& b) {
+    return (a.q_end - a.q_begin) > (b.q_end - b.q_begin);
+  });
+}
+
+void build_seg_lo(const Batch& bt, std::vector<int32_t>* out) {
+  out->assign(bt.sumT, -1);
+  for (const Row& r : bt.rows)
+    for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_start(r, t);
+}
+
+struct LPlan {
+  std::vector<LogitRowItem> rows;
+  std::vector<int32_t> labels;
+  std::vector<RespItem> resp;
+};
+
+void build_lplan(const Batch& bt, LPlan* out) {
+  out->rows.clear();
+  out->labels.clear();
+  out->resp.clear();
+  for (int b = 0; b < bt.B; ++b) {
+    const Row& r = bt.rows[b];
+    bool any = false;
+    for (int k = 0; k < r.K; ++k) any = any || r.len[k] > 0;
+    if (any) {
+      // the last prompt position predicts the first token of every response
+      LogitRowItem it{};
+      it.logit_row = (int64_t)r.tok0 + r.P - 1;
+      it.label_off = (int32_t)out->labels.size();
+      for (int k = 0; k < r.K; ++k)
+        if (r.len[k] > 0) out->labels.push_back(r.tok0 + r.off[k]);
+      it.label_cnt = (int32_t)out->labels.size() - it.label_off;
+      out->rows.push_back(it);
+      for (int k = 0; k < r.K; ++k) {
+        for (int32_t j = 1; j < r.len[k]; ++j) {
+          LogitRowItem e{};
+          e.logit_row = (int64_t)r.tok0 + r.off[k] + j - 1;
+          e.label_off = (int32_t)out->labels.size();
+          e.label_cnt = 1;
+          out->labels.push_back(r.tok0 + r.off[k] + j);
+          out->rows.push_back(e);
+        }
+      }
+    }
+    for (int k = 0; k < bt.Kmax; ++k) {
+      RespItem ri{};
+      ri.out = b * bt.Kmax + k;
+      if (k < r.K) {
+        ri.tok_begin = r.tok0 + r.off[k];
+        ri.len = r.len[k];
+      }
+      out->resp.push_back(ri);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Workspace layout: a metadata prefix copied from the host, then scratch
+// ---------------------------------------------------------------------------
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Region {
+  size_t off = 0, bytes = 0;
+};
+
+struct Layout {
+  std::vector<Region> regions;
+  size_t meta_bytes = 0;   // host-staged prefix
+  size_t total = 0;
+  size_t add(size_t bytes) {
+    Region r;
+    r.off = total;
+    r.bytes = bytes;
+    regions.push_back(r);
+    total = align_up(total + bytes);
+    return regions.size() - 1;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Pinned staging ring for plan metadata
+// ---------------------------------------------------------------------------
+
+struct StagingSlot {
+  void* host = nullptr;
+  size_t cap = 0;
+  hipEvent_t done = nullptr;
+  bool pending = false;
+};
+
+std::mutex g_stage_mu;
+StagingSlot g_stage[8];
+int g_stage_next = 0;
+
+struct StagingRelease {
+  ~StagingRelease() {
+    // Only free what is no longer in flight; the runtime may already be down at
+    // unload, in which case the OS reclaims the memory.
+    for (auto& s : g_stage) {
+      if (s.pending && s.done) hipEventSynchronize(s.done);
+      if (s.done) hipEventDestroy(s.done);
+      if (s.host) hipHostFree(s.host);
+      s = StagingSlot{};
+    }
+  }
+} g_stage_release;
+
+// Copies `bytes` from `src` into device memory `dst` through a pinned slot.
+pp_status stage_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return PP_OK;
+  std::lock_guard<std::mutex> lk(g_stage_mu);
+  StagingSlot& s = g_stage[g_stage_next];
+  g_stage_next = (g_stage_next + 1) % 8;
+  hipError_t e;
+  if (s.pending) {
+    e = hipEventSynchronize(s.done);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(staging)");
+    s.pending = false;
+  }
+  if (!s.done) {
+    e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate(staging)");
+  }
+  if (s.cap < bytes) {
+    if (s.host) hipHostFree(s.host);
+    s.host = nullptr;
+    s.cap = 0;
+    size_t cap = std::max<size_t>(bytes, 1 << 20);
+    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+    if (e != hipSuccess) return hip_fail(e, "hipHostMalloc(staging)");
+    s.cap = cap;
+  }
+  memcpy(s.host, src, bytes);
+  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(plan)");
+  e = hipEventRecord(s.done, stream);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+  s.pending = true;
+  return PP_OK;
+}
+
+// Serialises regions into one host image of the metadata prefix.
+struct MetaImage {
+  std::vector<uint8_t> buf;
+  void put(const Region& r, const void* src, size_t bytes) {
+    if (buf.size() < r.off + r.bytes) buf.resize(r.off + r.bytes);
+    if (bytes) memcpy(buf.data() + r.off, src, bytes);
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Attention plan + layout
+// ---------------------------------------------------------------------------
+
+struct FwdPlan {
+  QPlan q;
+  std::vector<int32_t> seg_lo;
+  Layout lay;
+  size_t r_seg, r_items, r_kt;
+};
+
+void plan_fwd(const Batch& bt, FwdPlan* p) {
+  build_qplan(bt, kFwdBlockM, kFwdBlockN, &p->q);
+  build_seg_lo(bt, &p->seg_lo);
+  p->lay = Layout();
+  p->r_seg = p->lay.add(p->seg_lo.size() * 4);
+  p->r_items = p->lay.add(p->q.items.size() * sizeof(QTileItem));
+  p->r_kt = p->lay.add(p->q.ktiles.size() * 4);
+  p->lay.meta_bytes = p->lay.total;
+}
+
+struct BwdPlan {
+  QPlan dq;
+  std::vector<KTileItem> kv;
+  std::vector<int32_t> seg_lo;
+  Layout lay;
+  size_t r_seg, r_dq_items, r_dq_kt, r_kv_items, r_delta;
+};
+
+void plan_bwd(const Batch& bt, int hq, BwdPlan* p) {
+  build_qplan(bt, kDqBlockM, kDqBlockN, &p->dq);
+  build_kplan(bt, kBwdBlockN, &p->kv);
+  build_seg_lo(bt, &p->seg_lo);
+  p->lay = Layout();
+  p->r_seg = p->lay.add(p->seg_lo.size() * 4);
+  p->r_dq_items = p->lay.add(p->dq.items.size() * sizeof(QTileItem));
+  p->r_dq_kt = p->lay.add(p->dq.ktiles.size() * 4);
+  p->r_kv_items = p->lay.add(p->kv.size() * sizeof(KTileItem));
+  p->lay.meta_bytes = p->lay.total;
+  p->r_delta = p->lay.add((size_t)hq * bt.sumT * 4);
+}
+
+struct LogprobPlan {
+  LPlan l;
+  Layout lay;
+  size_t r_rows, r_labels, r_resp, r_tok;
+};
+
+void plan_logprob(const Batch& bt, LogprobPlan* p) {
+  build_lplan(bt, &p->l);
+  p->lay = Layout();
+  p->r_rows = p->lay.add(p->l.rows.size() * sizeof(LogitRowItem));
+  p->r_labels = p->lay.add(p->l.labels.size() * 4);
+  p->r_resp = p->lay.add(p->l.resp.size() * sizeof(RespItem));
+  p->lay.meta_bytes = p->lay.total;
+  p->r_tok = p->lay.add((size_t)bt.sumT * 4);
+}
+
+pp_status check_logprob_layout(const Batch& bt) {
+  for (int b = 0; b < bt.B; ++b) {
+    const Row& r = bt.rows[b];
+    for (int k = 0; k < r.K; ++k)
+      if (r.len[k] > 0 && r.P == 0)
+        return fail(PP_ERR_BAD_LAYOUT,
+                    "row %d has an empty prompt and a non-empty response: its first token has no "
+                    "predicting position", b);
+  }
+  return PP_OK;
+}
+
+inline void* at(void* base, const Layout& lay, size_t region) {
+  return (uint8_t*)base + lay.regions[region].off;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel timing
+// ---------------------------------------------------------------------------
+
+struct TimingRec {
+  const char* name;
+  hipEvent_t start, stop;
+};
+
+std::mutex g_time_mu;
+std::atomic<bool> g_time_on{false};
+std::vector<TimingRec> g_time_pending;
+std::vector<hipEvent_t> g_event_pool;
+struct TimingTotal {
+  const char* name;
+  double ms;
+  int64_t launches;
+};
+std::vector<TimingTotal> g_time_totals;
+
+hipEvent_t pool_get() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void drain_timing_locked() {
+  for (auto& r : g_time_pending) {
+    float ms = 0.f;
+    hipEventSynchronize(r.stop);
+    hipEventElapsedTime(&ms, r.start, r.stop);
+    bool found = false;
+    for (auto& t : g_time_totals)
+      if (strcmp(t.name, r.name) == 0) {
+        t.ms += ms;
+        t.launches += 1;
+        found = true;
+      }
+    if (!found) g_time_totals.push_back({r.name, (double)ms, 1});
+    g_event_pool.push_back(r.start);
+    g_event_pool.push_back(r.stop);
+  }
+  g_time_pending.clear();
+}
+
+}  // namespace
+
+TimingScope::TimingScope(const char* name, hipStream_t stream) : slot_(-1), stream_(stream) {
+  if (!g_time_on.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  hipEvent_t a = pool_get(), b = pool_get();
+  if (!a || !b) return;
+  if (hipEventRecord(a, stream) != hipSuccess) return;
+  g_time_pending.push_back({name, a, b});
+  slot_ = (int)g_time_pending.size() - 1;
+}
+
+TimingScope::~TimingScope() {
+  if (slot_ < 0) return;
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  if (slot_ < (int)g_time_pending.size()) hipEventRecord(g_time_pending[slot_].stop, stream_);
+}
+
+}  // namespace pp
+
+using namespace pp;
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+
+extern "C" {
+
+int pp_version(void) { return 100; }
+
+const char* pp_status_string(pp_status s) {
+  switch (s) {
+    case PP_OK: return "ok";
+    case PP_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case PP_ERR_BAD_LAYOUT: return "bad packed layout";
+    case PP_ERR_UNSUPPORTED: return "unsupported";
+    case PP_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case PP_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char* pp_last_error(void) { return g_last_error.c_str(); }
+
+pp_status pp_workspace_size(const pp_pack_desc* desc, int hq, int hkv, int head_dim, int vocab,
+                            size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if (fwd || bwd) {
+    st = check_heads(hq, hkv, head_dim);
+    if (st != PP_OK) return st;
+  }
+  if (fwd) {
+    FwdPlan p;
+    plan_fwd(bt, &p);
+    *fwd = p.lay.total;
+  }
+  if (bwd) {
+    BwdPlan p;
+    plan_bwd(bt, hq, &p);
+    *bwd = p.lay.total;
+  }
+  if (logprob) {
+    if (vocab < 1) return fail(PP_ERR_INVALID_ARGUMENT, "vocab must be >= 1 for the logprob size");
+    st = check_logprob_layout(bt);
+    if (st != PP_OK) return st;
+    LogprobPlan p;
+    plan_logprob(bt, &p);
+    *logprob = p.lay.total;
+  }
+  if (loss) *loss = align_up((size_t)bt.B * 4);
+  return PP_OK;
+}
+
+pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      float scale, const void* q, const void* k, const void* v, void* o,
+                      float* lse, void* ws, size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
+    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
+  FwdPlan p;
+  plan_fwd(bt, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "forward needs %zu workspace bytes, got %zu", p.lay.total,
+                ws_bytes);
+  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (bt.sumT == 0) return PP_OK;
+  hipStream_t s = (hipStream_t)hip_stream;
+  MetaImage img;
+  img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
+  img.put(p.lay.regions[p.r_items], p.q.items.data(), p.q.items.size() * sizeof(QTileItem));
+  img.put(p.lay.regions[p.r_kt], p.q.ktiles.data(), p.q.ktiles.size() * 4);
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  AttnFwdLaunch a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.lse = lse;
+  a.items = (const QTileItem*)at(ws, p.lay, p.r_items);
+  a.ktiles = (const int32_t*)at(ws, p.lay, p.r_kt);
+  a.seg_lo = (const int32_t*)at(ws, p.lay, p.r_seg);
+  a.n_items = (int)p.q.items.size();
+  a.hq = hq;
+  a.hkv = hkv;
+  a.head_dim = head_dim;
+  a.sumT = bt.sumT;
+  a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
+  a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  hipError_t e = launch_attn_fwd(a, s);
+  if (e != hipSuccess) return hip_fail(e, "attention forward launch");
+  return PP_OK;
+}
+
+pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      float scale, const void* q, const void* k, const void* v, const void* o,
+                      const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
+                      size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
+    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
+  BwdPlan p;
+  plan_bwd(bt, hq, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", p.lay.total,
+                ws_bytes);
+  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (bt.sumT == 0) return PP_OK;
+  hipStream_t s = (hipStream_t)hip_stream;
+  MetaImage img;
+  img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
+  img.put(p.lay.regions[p.r_dq_items], p.dq.items.data(), p.dq.items.size() * sizeof(QTileItem));
+  img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * 4);
+  img.put(p.lay.regions[p.r_kv_items], p.kv.data(), p.kv.size() * sizeof(KTileItem));
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  AttnBwdLaunch a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.lse = lse;
+  a.dout = dout;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.delta = (float*)at(ws, p.lay, p.r_delta);
+  a.dq_items = (const QTileItem*)at(ws, p.lay, p.r_dq_items);
+  a.dq_ktiles = (const int32_t*)at(ws, p.lay, p.r_dq_kt);
+  a.n_dq_items = (int)p.dq.items.size();
+  a.kv_items = (const KTileItem*)at(ws, p.lay, p.r_kv_items);
+  a.n_kv_items = (int)p.kv.size();
+  a.seg_lo = (const int32_t*)at(ws, p.lay, p.r_seg);
+  a.hq = hq;
+  a.hkv = hkv;
+  a.head_dim = head_dim;
+  a.sumT = bt.sumT;
+  a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
+  a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  hipError_t e = launch_attn_bwd(a, s);
+  if (e != hipSuccess) return hip_fail(e, "attention backward launch");
+  return PP_OK;
+}
+
+pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                         const void* logits, const int32_t* tokens, float* seq_logp,
+                         float* tok_logp, void* ws, size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_dtype(logits_dtype)) != PP_OK) return st;
+  if (vocab < 1) return fail(PP_ERR_INVALID_ARGUMENT, "vocab must be >= 1");
+  if ((st = check_logprob_layout(bt)) != PP_OK) return st;
+  if (bt.Kmax > 0 && !seq_logp) return fail(PP_ERR_INVALID_ARGUMENT, "seq_logp is NULL");
+  if (bt.sumT > 0 && (!logits || !tokens))
+    return fail(PP_ERR_INVALID_ARGUMENT, "logits and tokens must be non-NULL");
+  LogprobPlan p;
+  plan_logprob(bt, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "logprob needs %zu workspace bytes, got %zu", p.lay.total,
+                ws_bytes);
+  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (bt.Kmax == 0 && (bt.sumT == 0 || !tok_logp)) return PP_OK;
+  hipStream_t s = (hipStream_t)hip_stream;
+  MetaImage img;
+  img.put(p.lay.regions[p.r_rows], p.l.rows.data(), p.l.rows.size() * sizeof(LogitRowItem));
+  img.put(p.lay.regions[p.r_labels], p.l.labels.data(), p.l.labels.size() * 4);
+  img.put(p.lay.regions[p.r_resp], p.l.resp.data(), p.l.resp.size() * sizeof(RespItem));
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  LogprobLaunch a{};
+  a.logits = logits;
+  a.tokens = tokens;
+  a.tok = tok_logp ? tok_logp : (float*)at(ws, p.lay, p.r_tok);
+  a.seq = seq_logp;
+  a.rows = (const LogitRowItem*)at(ws, p.lay, p.r_rows);
+  a.labels = (const int32_t*)at(ws, p.lay, p.r_labels);
+  a.resp = (const RespItem*)at(ws, p.lay, p.r_resp);
+  a.n_rows = (int)p.l.rows.size();
+  a.n_resp = (int)p.l.resp.size();
+  a.vocab = vocab;
+  a.sumT = bt.sumT;
+  a.dtype = logits_dtype == PP_FP32 ? kFP32 : kBF16;
+  hipError_t e = launch_logprob(a, s);
+  if (e != hipSuccess) return hip_fail(e, "logprob launch");
+  return PP_OK;
+}
+
+pp_status pp_dpo_loss(int32_t num_rows, int32_t max_resp, const int32_t* num_resp,
+                      const float* logp_pol, const float* logp_ref, float beta, float* loss,
+                      float* row_loss, float* dlogp_pol, void* ws, size_t ws_bytes,
+                      void* hip_stream) {
+  if (num_rows < 1) return fail(PP_ERR_INVALID_ARGUMENT, "num_rows must be >= 1");
+  if (max_resp < 0) return fail(PP_ERR_INVALID_ARGUMENT, "max_resp must be >= 0");
+  if (!num_resp || !logp_pol || !loss)
+    return fail(PP_ERR_INVALID_ARGUMENT, "num_resp, logp_pol and loss must be non-NULL");
+  if (!std::isfinite(beta)) return fail(PP_ERR_INVALID_ARGUMENT, "beta must be finite");
+  int qualified = 0;
+  for (int b = 0; b < num_rows; ++b) {
+    if (num_resp[b] < 0 || num_resp[b] > max_resp)
+      return fail(PP_ERR_INVALID_ARGUMENT, "num_resp[%d] = %d outside [0, %d]", b, num_resp[b], max_resp);
+    if (num_resp[b] >= 2) ++qualified;
+  }
+  if (qualified == 0) return fail(PP_ERR_INVALID_ARGUMENT, "no row has two responses to compare");
+  const size_t need = align_up((size_t)num_rows * 4);
+  if (ws_bytes < need)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "loss needs %zu workspace bytes, got %zu", need, ws_bytes);
+  if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  hipStream_t s = (hipStream_t)hip_stream;
+  pp_status st = stage_copy(ws, num_resp, (size_t)num_rows * 4, s);
+  if (st != PP_OK) return st;
+  LossLaunch a{};
+  a.num_resp = (const int32_t*)ws;
+  a.pol = logp_pol;
+  a.ref = logp_ref;
+  a.beta = beta;
+  a.loss = loss;
+  a.row_loss = row_loss;
+  a.dlogp = dlogp_pol;
+  a.B = num_rows;
+  a.K_max = max_resp;
+  a.n_qualified = qualified;
+  hipError_t e = launch_loss(a, s);
+  if (e != hipSuccess) return hip_fail(e, "loss launch");
+  return PP_OK;
+}
+
+pp_status pp_tile_class_len(const pp_pack_desc* desc, int block_q, int block_k, size_t* len) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if (block_q < 1 || block_k < 1) return fail(PP_ERR_INVALID_ARGUMENT, "block sizes must be >= 1");
+  if (!len) return fail(PP_ERR_INVALID_ARGUMENT, "len is NULL");
+  size_t n = 0;
+  for (const Row& r : bt.rows)
+    n += (size_t)((r.T + block_q - 1) / block_q) * ((r.T + block_k - 1) / block_k);
+  *len = n;
+  return PP_OK;
+}
+
+pp_status pp_pack_export(const pp_pack_desc* desc, int block_q, int block_k, int32_t* position_ids,
+                         int32_t* segment_ids, uint8_t* tile_class, size_t tile_class_len) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if (tile_class) {
+    size_t need = 0;
+    if ((st = pp_tile_class_len(desc, block_q, block_k, &need)) != PP_OK) return st;
+    if (tile_class_len < need)
+      return fail(PP_ERR_INVALID_ARGUMENT, "tile_class needs %zu entries, got %zu", need, tile_class_len);
+  }
+  size_t tc = 0;
+  for (const Row& r : bt.rows) {
+    for (int32_t t = 0; t < r.T; ++t) {
+      const int32_t sid = seg_id(r, t);
+      if (segment_ids) segment_ids[r.tok0 + t] = sid;
+      if (position_ids) {
+        int32_t pos = 0;
+        if (sid == 0) pos = t;
+        else if (sid > 0) pos = r.P + (t - r.off[sid - 1]);
+        position_ids[r.tok0 + t] = pos;
+      }
+    }
+    if (tile_class) {
+      for (int32_t q0 = 0; q0 < r.T; q0 += block_q)
+        for (int32_t k0 = 0; k0 < r.T; k0 += block_k)
+          tile_class[tc++] = classify_tile(r, q0, std::min(r.T, q0 + block_q), k0, std::min(r.T, k0 + block_k));
+    }
+  }
+  return PP_OK;
+}
+
+pp_status pp_timing_enable(int on) {
+  g_time_on.store(on != 0);
+  return PP_OK;
+}
+
+pp_status pp_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  drain_timing_locked();
+  g_time_totals.clear();
+  return PP_OK;
+}
+
+int pp_timing_count(void) {
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  drain_timing_locked();
+  return (int)g_time_totals.size();
+}
+
+pp_status pp_timing_get(int idx, const char** name, double* total_ms, int64_t* launches) {
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  drain_timing_locked();
+  if (idx < 0 || idx >= (int)g_time_totals.size())
+    return fail(PP_ERR_INVALID_ARGUMENT, "timing index %d out of range", idx);
+  if (name) *name = g_time_totals[idx].name;
+  if (total_ms) *total_ms = g_time_totals[idx].ms;
+  if (launches) *launches = g_time_totals[idx].launches;
+  return PP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+// Internal interface between the host entry points (pp_host.cpp) and the HIP
+// kernels.  Every launch wrapper enqueues on the given stream and returns the
+// HIP error of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pp_plan.h"
+
+namespace pp {
+
+enum ElemType { kBF16 = 0, kFP32 = 1 };
+
+// Brackets one kernel launch with hipEvents on its stream while timing is on.
+struct TimingScope {
+  TimingScope(const char* name, hipStream_t stream);
+  ~TimingScope();
+  TimingScope(const TimingScope&) = delete;
+  TimingScope& operator=(const TimingScope&) = delete;
+ private:
+  int slot_;
+  hipStream_t stream_;
+};
+
+struct AttnFwdLaunch {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  const QTileItem* items;
+  const int32_t* ktiles;
+  const int32_t* seg_lo;
+  int n_items;
+  int hq, hkv, head_dim;
+  int sumT;
+  float scale;
+  int dtype;
+};
+hipError_t launch_attn_fwd(const AttnFwdLaunch& a, hipStream_t s);
+
+struct AttnBwdLaunch {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* o;
+  const float* lse;
+  const void* dout;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* delta;              // [hq, sumT] scratch
+  const QTileItem* dq_items;
+  const int32_t* dq_ktiles;
+  int n_dq_items;
+  const KTileItem* kv_items;
+  int n_kv_items;
+  const int32_t* seg_lo;
+  int hq, hkv, head_dim;
+  int sumT;
+  float scale;
+  int dtype;
+};
+hipError_t launch_attn_bwd(const AttnBwdLaunch& a, hipStream_t s);
+
+struct LogprobLaunch {
+  const void* logits;
+  const int32_t* tokens;
+  float* tok;                // [sumT]; zero-filled, then response positions written
+  float* seq;                // [B * K_max]
+  const LogitRowItem* rows;
+  const int32_t* labels;     // flat token positions
+  const RespItem* resp;      // one per (b, k) slot
+  int n_rows;
+  int n_resp;
+  int vocab;
+  int sumT;
+  int dtype;
+};
+hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s);
+
+struct LossLaunch {
+  const int32_t* num_resp;   // device copy [B]
+  const float* pol;
+  const float* ref;          // may be null
+  float beta;
+  float* loss;
+  float* row_loss;           // may be null
+  float* dlogp;              // may be null
+  int B, K_max;
+  int n_qualified;           // rows with K_b >= 2
+};
+hipError_t launch_loss(const LossLaunch& a, hipStream_t s);
+
+}  // namespace pp

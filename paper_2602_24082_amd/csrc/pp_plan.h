@@ -1,0 +1,69 @@
+// Internal plan records shared by the host planner and the HIP kernels.
+//
+// A packed batch (prompt once, then K responses back to back, Sec. 3.2) is cut
+// into fixed-size query tiles (forward and dQ passes) and key tiles (dK/dV
+// pass).  For each tile the planner records where its row starts, the row's
+// prompt length and first padding position, and which tiles on the other side
+// hold at least one visible (query, key) pair.  The kernels decide per element
+// whether a pair is visible from three per-query integers:
+//
+//   visible(i, j) = (j <= hi_i) && (j < P || j >= lo_i)
+//
+// where i, j are row-relative, hi_i = i for real tokens and -1 for padding, and
+// lo_i is the row-relative start of the segment that holds i (0 in the prompt,
+// o_k in response k).  This is the mask of Sec. 3.2: causal, every token sees
+// the whole prompt, a response token sees only its own response besides it.
+#pragma once
+
+#include <stdint.h>
+
+namespace pp {
+
+// Tile sizes of the kernels (rows of the flat token axis).
+constexpr int kFwdBlockM = 128;   // queries per forward workgroup (4 waves x 32)
+constexpr int kFwdBlockN = 64;    // keys per forward k-tile
+constexpr int kDqBlockM = 128;    // queries per dQ workgroup
+constexpr int kDqBlockN = 64;     // keys per dQ k-tile
+constexpr int kBwdBlockN = 128;   // keys per dK/dV workgroup (4 waves x 32)
+constexpr int kBwdBlockM = 32;    // queries per dK/dV inner step
+
+// One query tile: queries [q0, q_end) of the row starting at flat index tok0.
+struct QTileItem {
+  int32_t tok0;    // flat index of the row's first token
+  int32_t q0;      // first query (row-relative)
+  int32_t q_end;   // one past the last query (row-relative, clipped to the row)
+  int32_t P;       // prompt length of the row
+  int32_t valid;   // first padding position (P + sum of response lengths)
+  int32_t kt_off;  // first entry of this tile's key-tile list
+  int32_t kt_cnt;  // number of key tiles with a visible pair
+  int32_t row;     // row index (diagnostics)
+};
+
+// One key tile: keys [k0, k_end) of a row and the query range that sees them.
+struct KTileItem {
+  int32_t tok0;
+  int32_t k0;
+  int32_t k_end;
+  int32_t P;
+  int32_t valid;
+  int32_t q_begin;  // first query that sees a key of the tile
+  int32_t q_end;    // one past the last such query
+  int32_t row;
+};
+
+// Gather record of the log-prob pass: one logit row and the labels it predicts.
+struct LogitRowItem {
+  int64_t logit_row;  // flat row of the logits matrix
+  int32_t label_off;  // first entry in the label list
+  int32_t label_cnt;  // number of labels predicted from this row
+};
+
+// Response record of the segmented sum.
+struct RespItem {
+  int32_t tok_begin;  // flat position of the response's first token
+  int32_t len;        // number of tokens
+  int32_t out;        // index into seq_logp (b * K_max + k)
+  int32_t pad;
+};
+
+}  // namespace pp

@@ -1,0 +1,163 @@
+"""Host-side tests of the C ABI: the library loads and exports every declared
+symbol, the planner's integer outputs equal the oracle's bit for bit, and bad
+arguments come back as error codes before anything touches a GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import pp_oracle as orc
+from paper_2602_24082_amd import binding
+from paper_2602_24082_amd import workload as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", fn)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names += re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\**\s+(pp_[a-z_]+)\s*\(", src, re.M)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    L = binding.lib()
+    declared = _declared_functions()
+    assert "pp_attn_fwd" in declared and "pp_dpo_loss" in declared
+    for name in declared:
+        assert hasattr(L, name), name
+    assert set(binding.EXPORTED) <= set(declared)
+
+
+def test_status_strings():
+    L = binding.lib()
+    for s in range(6):
+        assert L.pp_status_string(s)
+    assert L.pp_version() >= 100
+
+
+def _random_pack(rng, B=None, pad=True, zero_prompt_ok=True):
+    B = B or int(rng.integers(1, 5))
+    P = [int(rng.integers(0 if zero_prompt_ok else 1, 40)) for _ in range(B)]
+    L = [[int(x) for x in rng.integers(0, 30, size=int(rng.integers(0, 5)))] for _ in range(B)]
+    padv = [int(rng.integers(0, 9)) if pad else 0 for _ in range(B)]
+    return wl.make_pack(P, L, pad=padv)
+
+
+@pytest.mark.parametrize("bq,bk", [(1, 1), (2, 3), (16, 16), (32, 64), (128, 64), (128, 128), (7, 5)])
+def test_export_matches_oracle_bit_exact(bq, bk):
+    rng = np.random.default_rng(bq * 1000 + bk)
+    for _ in range(8):
+        pack = _random_pack(rng)
+        pos, seg, tiles = binding.pp_pack_export(pack, bq, bk)
+        args = pack.oracle_args()
+        assert (pos == orc.pack_position_ids(*args)).all()
+        assert (seg == orc.pack_segment_ids(*args)).all()
+        assert (tiles == orc.pack_tile_classes(*args, bq, bk)).all()
+
+
+def test_export_golden_fixture_row():
+    pack = wl.make_pack([3], [[2, 2]], pad=[1])
+    pos, seg, tiles = binding.pp_pack_export(pack, 2, 2)
+    assert pos.tolist() == [0, 1, 2, 3, 4, 3, 4, 0]
+    assert seg.tolist() == [0, 0, 0, 1, 1, 2, 2, -1]
+    assert tiles.reshape(4, 4).tolist() == [[1, 0, 0, 0], [2, 1, 0, 0], [2, 1, 1, 0], [1, 1, 1, 1]]
+
+
+def test_export_config_sized_rows():
+    """Full-size rows of the 8B-shaped workload at the kernels' own tile sizes."""
+    pack = wl.config_pack(wl.CONFIGS[1], rows=2)
+    for bq, bk in [(128, 64), (32, 128)]:
+        _, _, tiles = binding.pp_pack_export(pack, bq, bk)
+        assert (tiles == orc.pack_tile_classes(*pack.oracle_args(), bq, bk)).all()
+
+
+# ------------------------------------------------------------- error codes
+
+
+def _raw_desc(row_start, prompt, num, off, ln, kmax):
+    arrs = [np.asarray(x, np.int32) for x in (row_start, prompt, num, off, ln)]
+    ptr = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    d = binding._Desc(len(prompt), kmax, *[ptr(a) for a in arrs])
+    return d, arrs
+
+
+def _fwd_status(desc, hq=4, hkv=2, d=64, dtype=0):
+    L = binding.lib()
+    fake = ctypes.c_void_p(16)  # never dereferenced: validation fails first
+    return L.pp_attn_fwd(ctypes.byref(desc), dtype, hq, hkv, d, 0.0, fake, fake, fake, fake, fake,
+                         fake, 1 << 30, None)
+
+
+def test_bad_layouts_are_rejected_before_launch():
+    good, a = _raw_desc([0, 10], [4], [2], [4, 7], [3, 3], 2)
+    cases = [
+        (_raw_desc([0, 10], [4], [2], [4, 8], [3, 2], 2), 2),     # gap between responses
+        (_raw_desc([0, 10], [4], [2], [5, 8], [3, 2], 2), 2),     # first response not at P
+        (_raw_desc([0, 8], [4], [2], [4, 7], [3, 3], 2), 2),      # overflows the row
+        (_raw_desc([0, 10], [-1], [0], [0, 0], [0, 0], 2), 2),    # negative prompt
+        (_raw_desc([0, 10], [4], [3], [4, 7], [3, 3], 2), 2),     # more responses than max
+        (_raw_desc([0, 10], [4], [2], [4, 4], [-1, 3], 2), 2),    # negative length
+        (_raw_desc([1, 10], [4], [0], [0, 0], [0, 0], 2), 2),     # row_start[0] != 0
+        (_raw_desc([0, 10, 5], [4, 0], [0, 0], [0, 0, 0, 0], [0, 0, 0, 0], 2), 2),  # decreasing
+    ]
+    for (d, keep), want in cases:
+        assert _fwd_status(d) == want, binding.lib().pp_last_error()
+        assert binding.lib().pp_last_error()
+
+
+def test_bad_heads_and_dims():
+    d, keep = _raw_desc([0, 10], [4], [2], [4, 7], [3, 3], 2)
+    assert _fwd_status(d, hq=4, hkv=3) == 1
+    assert _fwd_status(d, hq=0, hkv=1) == 1
+    assert _fwd_status(d, d=96) == 3
+    assert _fwd_status(d, d=256) == 3
+    assert _fwd_status(d, dtype=7) == 1
+
+
+def test_workspace_too_small_and_nulls():
+    L = binding.lib()
+    d, keep = _raw_desc([0, 10], [4], [2], [4, 7], [3, 3], 2)
+    fake = ctypes.c_void_p(16)
+    st = L.pp_attn_fwd(ctypes.byref(d), 0, 4, 2, 64, 0.0, fake, fake, fake, fake, fake, fake, 1, None)
+    assert st == 4
+    st = L.pp_attn_fwd(ctypes.byref(d), 0, 4, 2, 64, 0.0, None, fake, fake, fake, fake, fake, 1 << 30, None)
+    assert st == 1
+    assert L.pp_attn_fwd(None, 0, 4, 2, 64, 0.0, fake, fake, fake, fake, fake, fake, 1 << 30, None) == 1
+
+
+def test_logprob_needs_a_prompt():
+    L = binding.lib()
+    d, keep = _raw_desc([0, 5], [0], [1], [0], [5], 1)
+    fake = ctypes.c_void_p(16)
+    st = L.pp_seq_logprob(ctypes.byref(d), 0, 100, fake, fake, fake, None, fake, 1 << 30, None)
+    assert st == 2
+    # the same row is fine for attention (document-masked packing)
+    assert binding.pp_workspace_size(wl.make_pack([0], [[5]]), 2, 1, 64)[0] > 0
+
+
+def test_loss_argument_checks():
+    L = binding.lib()
+    fake = ctypes.c_void_p(16)
+    nr = np.array([1, 0], np.int32)
+    st = L.pp_dpo_loss(2, 2, ctypes.c_void_p(nr.ctypes.data), fake, None, 0.1, fake, None, None, fake, 4096, None)
+    assert st == 1  # no row with two responses
+    nr = np.array([3, 2], np.int32)
+    st = L.pp_dpo_loss(2, 2, ctypes.c_void_p(nr.ctypes.data), fake, None, 0.1, fake, None, None, fake, 4096, None)
+    assert st == 1  # num_resp above max_resp
+    nr = np.array([2, 2], np.int32)
+    st = L.pp_dpo_loss(2, 2, ctypes.c_void_p(nr.ctypes.data), fake, None, 0.1, fake, None, None, fake, 4, None)
+    assert st == 4  # workspace
+
+
+def test_workspace_sizes_grow_with_batch():
+    small = wl.config_pack(wl.CONFIGS[0])
+    big = wl.config_pack(wl.CONFIGS[1])
+    a = binding.pp_workspace_size(small, 4, 4, 64, 1000, logprob=True)
+    b = binding.pp_workspace_size(big, 32, 8, 128, 128256, logprob=True)
+    assert all(x > 0 for x in a) and all(y >= x for x, y in zip(a, b))

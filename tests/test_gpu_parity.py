@@ -1,0 +1,207 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerances (attention in bf16 MFMA with fp32 accumulation):
+  O            max |O - O_ref|                          <= 1e-2
+  LSE          max |lse - lse_ref|                      <= 1e-2
+  dQ, dK, dV   ||g - g_ref||_F / ||g_ref||_F            <= 2e-2 (each)
+  seq log-prob |s - s_ref| / |s_ref|                    <= 1e-4
+  loss, dlogp  relative                                 <= 1e-4
+The oracle runs on the inputs the kernels see: bf16 inputs as rounded, fp32
+inputs as given (the kernels round them to bf16 at load, which the bf16
+tolerances cover).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import pp_oracle as orc
+from paper_2602_24082_amd import binding as pp
+from paper_2602_24082_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+O_TOL = 1e-2
+LSE_TOL = 1e-2
+G_TOL = 2e-2
+LP_TOL = 1e-4
+
+
+def _inputs(pack, hq, hkv, d, dtype, seed):
+    q, k, v, do = wl.qkv(pack, hq, hkv, d, seed, dtype, device="cpu")
+    return q, k, v, do
+
+
+def _rel_fro(a, b):
+    n = np.linalg.norm(b)
+    return np.linalg.norm(a - b) / max(n, 1e-30)
+
+
+def _poisoned_like(t):
+    return torch.full_like(t, float("nan"))
+
+
+def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True):
+    print(f"case rows={pack.num_rows} T={pack.total_tokens} hq={hq} hkv={hkv} d={d} {dtype} seed={seed}",
+          flush=True)
+    q, k, v, do = _inputs(pack, hq, hkv, d, dtype, seed)
+    qg, kg, vg, dog = (x.to(DEV) for x in (q, k, v, do))
+    T = pack.total_tokens
+    o = _poisoned_like(qg)
+    lse = torch.full((hq, T), float("nan"), device=DEV)
+    pp.pp_attn_fwd(pack, qg, kg, vg, out=o, lse=lse)
+    args = pack.oracle_args()
+    qn, kn, vn, don = (x.double().numpy() for x in (q, k, v, do))
+    O_ref, L_ref = orc.attn_fwd(*args, qn, kn, vn)
+    o_c = o.double().cpu().numpy()
+    l_c = lse.double().cpu().numpy()
+    assert np.isfinite(o_c).all() and np.isfinite(l_c).all(), "unwritten output"
+    assert np.abs(o_c - O_ref).max() <= O_TOL, np.abs(o_c - O_ref).max()
+    assert np.abs(l_c - L_ref).max() <= LSE_TOL, np.abs(l_c - L_ref).max()
+    if not check_bwd:
+        return
+    dq, dk, dv = _poisoned_like(qg), _poisoned_like(kg), _poisoned_like(vg)
+    pp.pp_attn_bwd(pack, qg, kg, vg, o, lse, dog, dq=dq, dk=dk, dv=dv)
+    dq_r, dk_r, dv_r = orc.attn_bwd(*args, qn, kn, vn, don)
+    for name, got, ref in (("dq", dq, dq_r), ("dk", dk, dk_r), ("dv", dv, dv_r)):
+        g = got.double().cpu().numpy()
+        assert np.isfinite(g).all(), f"unwritten {name}"
+        err = _rel_fro(g, ref)
+        assert err <= G_TOL, (name, err)
+    # padding rows are exactly zero
+    seg = orc.pack_segment_ids(*args)
+    pad = seg < 0
+    if pad.any():
+        assert (o_c[pad] == 0).all() and (l_c[:, pad] == 0).all()
+        assert (dq.cpu().double().numpy()[pad] == 0).all()
+        assert (dk.cpu().double().numpy()[pad] == 0).all()
+        assert (dv.cpu().double().numpy()[pad] == 0).all()
+
+
+def test_tiny_fp32_config():
+    """4 rows, 4 heads (MHA), d 64, fp32 inputs, K=2 (the tiny check config)."""
+    cfg = wl.CONFIGS[0]
+    _check_attention(wl.config_pack(cfg), cfg.hq, cfg.hkv, cfg.head_dim, torch.float32, 11)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_bf16_gqa_ragged(d):
+    """Several tiles per row, unaligned boundaries, padding, GQA 8/2."""
+    pack = wl.make_pack([300, 0, 129, 5, 64], [[70, 45], [33, 64], [1, 0, 200], [130], [64, 64]],
+                        pad=[3, 0, 0, 17, 0])
+    _check_attention(pack, 8, 2, d, torch.bfloat16, 21 + d)
+
+
+def test_bf16_k4_mha():
+    pack = wl.make_pack([200, 57], [[31, 64, 1, 97], [128, 2, 300, 9]], pad=[0, 40])
+    _check_attention(pack, 4, 4, 128, torch.bfloat16, 31)
+
+
+def test_edge_cases():
+    """Single response (plain causal), empty prompt (document masking), one-token
+    rows, empty rows, all-padding rows, rows shorter than one tile."""
+    pack = wl.make_pack([0, 1, 7, 0, 129, 3, 0],
+                        [[1], [], [0, 0], [], [], [1, 1, 1], [5, 6]],
+                        pad=[0, 0, 0, 0, 0, 2, 0])
+    _check_attention(pack, 4, 1, 64, torch.bfloat16, 41)
+    pack = wl.make_pack([5, 0], [[], []], pad=[0, 9])  # all-padding second row
+    _check_attention(pack, 2, 2, 128, torch.bfloat16, 42)
+
+
+def test_g8_long_prefix_small():
+    """64/8-style grouping (G=8) with a long prefix and short responses."""
+    pack = wl.make_pack([700, 450], [[64, 100], [256, 70]])
+    _check_attention(pack, 16, 2, 128, torch.bfloat16, 51)
+
+
+def test_backward_is_deterministic():
+    pack = wl.make_pack([400, 150], [[100, 61], [33, 270]])
+    q, k, v, do = (x.to(DEV) for x in _inputs(pack, 8, 2, 128, torch.bfloat16, 61))
+    o, lse = pp.pp_attn_fwd(pack, q, k, v)
+    g1 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+    g2 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+    o2, lse2 = pp.pp_attn_fwd(pack, q, k, v)
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
+
+
+# ---------------------------------------------------------------- log-prob / loss
+
+
+def _check_logprob(pack, V, dtype, sigma, seed):
+    print(f"logprob rows={pack.num_rows} T={pack.total_tokens} V={V} {dtype}", flush=True)
+    T = pack.total_tokens
+    logits = wl.randn((T, V), seed, dtype, "cpu", sigma=sigma)
+    tokens = wl.randint((T,), V, seed + 1, "cpu")
+    seq = torch.full((pack.num_rows, pack.max_resp), float("nan"), device=DEV)
+    tok = torch.full((T,), float("nan"), device=DEV)
+    pp.pp_seq_logprob(pack, logits.to(DEV), tokens.to(DEV), want_tok=True, seq=seq, tok=tok)
+    ref_seq, ref_tok = orc.seq_logprob(*pack.oracle_args(), logits.double().numpy(), tokens.numpy())
+    s = seq.double().cpu().numpy()
+    t = tok.double().cpu().numpy()
+    assert np.isfinite(s).all() and np.isfinite(t).all()
+    nz = np.abs(ref_seq) > 0
+    assert (s[~nz] == 0).all()
+    rel = np.abs(s[nz] - ref_seq[nz]) / np.abs(ref_seq[nz])
+    assert rel.max() <= LP_TOL, rel.max()
+    assert np.abs(t - ref_tok).max() <= 1e-4 * max(1.0, np.abs(ref_tok).max())
+    return s
+
+
+def test_logprob_tiny_fp32():
+    cfg = wl.CONFIGS[0]
+    _check_logprob(wl.config_pack(cfg), 1000, torch.float32, 2.0, 71)
+
+
+def test_logprob_bf16_odd_vocab_and_edges():
+    # vocab 4099: rows are not 16-byte aligned -> element path; empty responses
+    pack = wl.make_pack([5, 1, 9], [[3, 0, 7], [1], [12, 40]], pad=[2, 0, 1])
+    _check_logprob(pack, 4099, torch.bfloat16, 3.0, 72)
+    _check_logprob(pack, 4096, torch.bfloat16, 3.0, 73)
+
+
+def test_logprob_bf16_llama_vocab():
+    pack = wl.make_pack([40, 17], [[9, 30, 2, 11], [25, 1, 0, 8]])
+    _check_logprob(pack, 128256, torch.bfloat16, 3.0, 74)
+
+
+def test_logprob_out_of_range_label_poisons_response():
+    pack = wl.make_pack([4], [[3, 3]])
+    V = 64
+    logits = wl.randn((10, V), 80, torch.float32, "cpu")
+    tokens = wl.randint((10,), V, 81, "cpu")
+    tokens[5] = V + 3  # inside response 0
+    seq = pp.pp_seq_logprob(pack, logits.to(DEV), tokens.to(DEV)).cpu()
+    assert math.isnan(seq[0, 0]) and math.isfinite(seq[0, 1])
+
+
+def _check_loss(num, pol, ref, beta):
+    polg = torch.tensor(pol, dtype=torch.float32, device=DEV)
+    refg = None if ref is None else torch.tensor(ref, dtype=torch.float32, device=DEV)
+    loss, rows, grad = pp.pp_dpo_loss(num, polg, refg, beta)
+    want, want_rows, want_g = orc.pair_loss(num, np.asarray(pol, np.float32).astype(np.float64),
+                                            None if ref is None else np.asarray(ref, np.float32).astype(np.float64),
+                                            beta)
+    assert abs(float(loss) - want) <= LP_TOL * abs(want)
+    assert np.allclose(rows.cpu().numpy(), want_rows, rtol=LP_TOL, atol=1e-7)
+    assert np.allclose(grad.cpu().numpy(), want_g, rtol=LP_TOL, atol=1e-8)
+
+
+def test_dpo_loss_and_bt_loss():
+    rng = np.random.default_rng(90)
+    _check_loss([2, 2, 2, 2], rng.standard_normal((4, 2)) * 30, rng.standard_normal((4, 2)) * 30, 0.1)
+    _check_loss([4, 3, 1, 4, 0, 2], rng.standard_normal((6, 4)) * 10, None, 1.0)
+    B = 700  # more rows than threads
+    _check_loss(list(rng.integers(0, 5, B)), rng.standard_normal((B, 4)) * 5, rng.standard_normal((B, 4)) * 5, 0.5)
+
+
+def test_full_chain_tiny_config():
+    """Tiny config end to end: policy and reference log-probs, then DPO at beta 0.1."""
+    cfg = wl.CONFIGS[0]
+    pack = wl.config_pack(cfg)
+    s_pol = _check_logprob(pack, cfg.vocab, torch.float32, cfg.logit_sigma, 100)
+    s_ref = _check_logprob(pack, cfg.vocab, torch.float32, cfg.logit_sigma, 200)
+    _check_loss(pack.num_resp.tolist(), s_pol, s_ref, cfg.beta)
