@@ -1,0 +1,306 @@
+"""Benchmark of the preference-packing hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1]
+
+One step = one pass of the whole hot path over one packed batch of the
+Llama-3-8B-shaped workload (8 rows, 32 query / 8 kv heads, head_dim 128, prompt
+U[256,1536], K=2 responses U[64,512], bf16):
+
+    plan -> attention forward -> attention backward (dQ, dK, dV)
+         -> per-response log-probs of policy and reference logits
+            (Llama-3 vocabulary 128256, bf16) -> DPO loss (beta 0.1)
+
+The headline value is the attention's useful throughput: only visible
+(query, key) pairs count, 4*d*Hq per pair forward and 10*d*Hq backward
+(the FlashAttention convention), divided by the attention's own time inside
+the timed steps (HIP events on the stream).  Printed as ONE JSON line, with the
+roofline of the dominant kernel (its algorithmic FLOPs or bytes per launch over
+its average launch time, from the library's per-launch HIP events), the oracle
+timed on the host cores on a bounded sample, and the speedup over the same
+kernels on the unpacked, prompt-duplicated, padded layout.
+
+    python bench.py --calib-copy      # plain device copy of known size, for
+                                      # scaling rocprofv3 FETCH_SIZE/WRITE_SIZE
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2602_24082_amd import binding as pp  # noqa: E402
+from paper_2602_24082_amd import workload as wl  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA (vendor, 2.4 GHz)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (vendor)
+LOGPROB_VOCAB = 128256      # Llama-3 vocabulary for the 8B-shaped workload
+LOGPROB_SIGMA = 3.0
+DPO_BETA = 0.1
+
+
+def useful_pairs(pack: wl.Pack) -> int:
+    """Visible (query, key) pairs: P(P+1)/2 + sum_k [L_k P + L_k(L_k+1)/2] per row."""
+    n = 0
+    for b in range(pack.num_rows):
+        P = int(pack.prompt_len[b])
+        n += P * (P + 1) // 2
+        for k in range(int(pack.num_resp[b])):
+            L = int(pack.resp_len[b, k])
+            n += L * P + L * (L + 1) // 2
+    return n
+
+
+def logit_rows_needed(pack: wl.Pack) -> int:
+    n = 0
+    for b in range(pack.num_rows):
+        lens = [int(pack.resp_len[b, k]) for k in range(int(pack.num_resp[b]))]
+        if any(L > 0 for L in lens):
+            n += 1 + sum(max(L - 1, 0) for L in lens)
+    return n
+
+
+class Attn:
+    """Inputs, outputs and workspaces of one attention fwd+bwd on a pack."""
+
+    def __init__(self, pack, hq, hkv, d, seed, dev):
+        self.pack = pack
+        self.q, self.k, self.v, self.do = wl.qkv(pack, hq, hkv, d, seed, torch.bfloat16, dev)
+        T = pack.total_tokens
+        self.o = torch.empty_like(self.q)
+        self.lse = torch.empty(hq, T, dtype=torch.float32, device=dev)
+        self.dq = torch.empty_like(self.q)
+        self.dk = torch.empty_like(self.k)
+        self.dv = torch.empty_like(self.v)
+        f, b, _, _ = pp.pp_workspace_size(pack, hq, hkv, d, fwd=True, bwd=True, loss=False)
+        self.ws_f = torch.empty(max(f, 1), dtype=torch.uint8, device=dev)
+        self.ws_b = torch.empty(max(b, 1), dtype=torch.uint8, device=dev)
+
+    def run(self):
+        pp.pp_attn_fwd(self.pack, self.q, self.k, self.v, out=self.o, lse=self.lse, ws=self.ws_f)
+        pp.pp_attn_bwd(self.pack, self.q, self.k, self.v, self.o, self.lse, self.do, dq=self.dq,
+                       dk=self.dk, dv=self.dv, ws=self.ws_b)
+
+
+def time_attention(pack, hq, hkv, d, dev, iters=10, warmup=3):
+    a = Attn(pack, hq, hkv, d, 977, dev)
+    for _ in range(warmup):
+        a.run()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(iters):
+        a.run()
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / iters
+    del a
+    torch.cuda.empty_cache()
+    return ms
+
+
+def cpu_baseline(pack, cfg, rows, seed):
+    """The oracle (fp64 numpy) on a bounded sample of the same workload: the
+    attention forward and backward of the given rows, all heads."""
+    from oracle import pp_oracle as orc
+    from threadpoolctl import threadpool_info
+    flops = 0
+    secs = 0.0
+    for b in rows:
+        one = wl.make_pack([int(pack.prompt_len[b])], [pack.resp_len[b, :int(pack.num_resp[b])].tolist()])
+        q, k, v, do = wl.qkv(one, cfg.hq, cfg.hkv, cfg.head_dim, seed + b, torch.bfloat16, "cpu")
+        qn, kn, vn, don = (x.double().numpy() for x in (q, k, v, do))
+        args = one.oracle_args()
+        t0 = time.perf_counter()
+        orc.attn_fwd(*args, qn, kn, vn)
+        orc.attn_bwd(*args, qn, kn, vn, don)
+        secs += time.perf_counter() - t0
+        flops += 14 * cfg.head_dim * cfg.hq * useful_pairs(one)
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": flops / secs / 1e12, "unit": "useful TFLOP/s (attention fwd+bwd)",
+            "cores": int(threads), "kind": "oracle",
+            "sample": (f"rows {list(rows)} of the benchmarked batch (T={[int(pack.row_lengths()[b]) for b in rows]}), "
+                       f"all {cfg.hq} heads, attention fwd+bwd in fp64 numpy, {secs:.1f} s; "
+                       f"host has {len(os.sched_getaffinity(0))} usable cores")}
+
+
+def calib_copy(dev):
+    """A plain device copy of 1 GiB, five times: read 1 GiB + write 1 GiB each."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calib_copy_bytes": n, "launches": 5}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-comparator", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the packed rows shard by "
+              "data parallelism with no exchange, so multi-GPU throughput is N x this line)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    if args.calib_copy:
+        calib_copy(dev)
+        return
+
+    cfg = wl.CONFIGS[args.config]
+    pack = wl.config_pack(cfg)
+    T = pack.total_tokens
+    seed = wl.tensor_seed(cfg.index, 0)
+    attn = Attn(pack, cfg.hq, cfg.hkv, cfg.head_dim, seed, dev)
+    V = cfg.vocab or LOGPROB_VOCAB
+    sigma = cfg.logit_sigma if cfg.vocab else LOGPROB_SIGMA
+    logits_pol = wl.randn_rows(T, V, seed + wl.STREAM_LOGITS_POL, torch.bfloat16, dev, sigma)
+    logits_ref = wl.randn_rows(T, V, seed + wl.STREAM_LOGITS_REF, torch.bfloat16, dev, sigma)
+    tokens = wl.randint((T,), V, seed + wl.STREAM_TOKENS, dev)
+    Kmax = pack.max_resp
+    seq_pol = torch.empty(pack.num_rows, Kmax, dtype=torch.float32, device=dev)
+    seq_ref = torch.empty_like(seq_pol)
+    lp_ws_n = pp.pp_workspace_size(pack, vocab=V, fwd=False, bwd=False, logprob=True, loss=True)
+    ws_lp = torch.empty(lp_ws_n[2], dtype=torch.uint8, device=dev)
+    ws_loss = torch.empty(max(lp_ws_n[3], 256), dtype=torch.uint8, device=dev)
+    num_resp = pack.num_resp.tolist()
+    beta = cfg.beta if cfg.vocab else DPO_BETA
+    with_ref = cfg.with_ref if cfg.vocab else True
+
+    attn_ev = []
+
+    def step(record):
+        if record:
+            a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a0.record()
+        attn.run()
+        if record:
+            a1.record()
+            attn_ev.append((a0, a1))
+        pp.pp_seq_logprob(pack, logits_pol, tokens, seq=seq_pol, ws=ws_lp)
+        if with_ref:
+            pp.pp_seq_logprob(pack, logits_ref, tokens, seq=seq_ref, ws=ws_lp)
+        return pp.pp_dpo_loss(num_resp, seq_pol, seq_ref if with_ref else None, beta, ws=ws_loss)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        loss, _, _ = step(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pp.pp_timing_enable(False)
+    kern = pp.pp_timing_get()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    attn_ms = sum(a.elapsed_time(b) for a, b in attn_ev) / args.steps
+    loss_val = float(loss.item())
+
+    U = useful_pairs(pack)
+    d, hq = cfg.head_dim, cfg.hq
+    fwd_flops = 4 * d * hq * U
+    bwd_flops = 10 * d * hq * U
+    useful = fwd_flops + bwd_flops
+    tflops = useful / (attn_ms * 1e-3) / 1e12
+
+    # algorithmic work per launch of each kernel (FLOPs of the GEMMs its algorithm
+    # performs, or bytes it must move)
+    n_rows = logit_rows_needed(pack)
+    per_launch = {
+        "pp_attn_fwd": ("mfma", 4 * d * hq * U),
+        "pp_attn_bwd_dkdv": ("mfma", 8 * d * hq * U),
+        "pp_attn_bwd_dq": ("mfma", 6 * d * hq * U),
+        "pp_logprob_rows": ("hbm", n_rows * V * 2 + n_rows * 16),
+    }
+    dom = max((k for k in kern if k in per_launch), key=lambda k: kern[k][0])
+    bound, work = per_launch[dom]
+    avg_ms = kern[dom][0] / kern[dom][1]
+    if bound == "mfma":
+        ach = work / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "avg_launch_ms": round(avg_ms, 4)}
+    else:
+        ach = work / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                "avg_launch_ms": round(avg_ms, 4)}
+    kernels = {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in kern.items()}
+    lp = kern.get("pp_logprob_rows")
+    logprob = None
+    if lp:
+        lp_ms = lp[0] / lp[1]
+        gbs = (n_rows * V * 2 + n_rows * 16) / (lp_ms * 1e-3) / 1e9
+        logprob = {"kernel": "pp_logprob_rows", "GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                   "rows": n_rows, "vocab": V, "avg_ms": round(lp_ms, 4)}
+
+    comp = None
+    if not args.no_comparator:
+        padded = wl.unpacked_padded(pack)
+        varlen = wl.unpacked_varlen(pack)
+        t_packed = time_attention(pack, hq, cfg.hkv, d, dev)
+        t_pad = time_attention(padded, hq, cfg.hkv, d, dev)
+        t_var = time_attention(varlen, hq, cfg.hkv, d, dev)
+        comp = {"packed_ms": round(t_packed, 4), "unpacked_padded_ms": round(t_pad, 4),
+                "unpacked_varlen_ms": round(t_var, 4),
+                "speedup_vs_padded": round(t_pad / t_packed, 3),
+                "speedup_vs_varlen": round(t_var / t_packed, 3),
+                "padded_layout": f"{padded.num_rows} sequences x {int(padded.row_lengths()[0])} tokens"}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(pack, cfg, list(range(pack.num_rows)), seed)
+
+    out = {
+        "metric": "packed attn fwd+bwd useful TFLOP/s (% bf16 peak); speedup vs unpacked padded",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "attn_ms_per_step": round(attn_ms, 4),
+        "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "rows": pack.num_rows, "tokens": T, "hq": hq, "hkv": cfg.hkv,
+                   "head_dim": d, "useful_pairs": U, "logprob_vocab": V, "beta": beta,
+                   "parallelism": "none (1 GPU)"},
+        "speedup_vs_padded": comp["speedup_vs_padded"] if comp else None,
+        "comparator": comp,
+        "logprob": logprob,
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "loss": loss_val,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()
