@@ -74,7 +74,7 @@ typedef enum pp_status {
 
 typedef enum pp_dtype {
   PP_BF16 = 0,  /* bfloat16 */
-  PP_FP32 = 1   /* float; attention rounds it to bf16 (nearest even) at tile load */
+  PP_FP32 = 1   /* float; attention inputs are rounded to bf16 (nearest even) */
 } pp_dtype;
 
 /* Host description of a packed batch; see "The packed layout" above. */
@@ -89,19 +89,21 @@ typedef struct pp_pack_desc {
 } pp_pack_desc;
 
 /* Device workspace (bytes) that each entry point needs for this batch.
- * Any output pointer may be NULL.  vocab is used only for logprob and may be 0.
- * hq, hkv and head_dim are validated as for pp_attn_fwd when fwd or bwd is
- * requested.  loss is the workspace of pp_dpo_loss for this batch's B. */
-pp_status pp_workspace_size(const pp_pack_desc* desc, int hq, int hkv, int head_dim, int vocab,
-                            size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss);
+ * Any output pointer may be NULL.  dtype is the attention input dtype (fp32
+ * inputs need room for their bf16 copies).  vocab is used only for logprob and
+ * may be 0.  hq, hkv and head_dim are validated as for pp_attn_fwd when fwd or
+ * bwd is requested.  loss is the workspace of pp_dpo_loss for this batch's B. */
+pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                            int vocab, size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss);
 
 /* Forward packed attention (Sec. 3.2): for every non-padding query i and head h
  *   O[i,h]   = sum_j softmax_j(scale * q[i,h] . k[j,g]) v[j,g] over the keys j
  *              that query i sees, g = h / (hq/hkv);
  *   lse[h,i] = ln sum_j exp(scale * q[i,h] . k[j,g]).
  * Padding queries get O = 0 and lse = 0.
- * dtype: PP_BF16 or PP_FP32 for q, k, v and o (fp32 is rounded to bf16 on load;
- * products accumulate in fp32).  head_dim in {64, 128}; hq % hkv == 0.
+ * dtype: PP_BF16 or PP_FP32 for q, k, v and o (fp32 inputs are rounded to bf16,
+ * nearest even, into the workspace first; products accumulate in fp32).
+ * head_dim in {64, 128}; hq % hkv == 0.
  * scale <= 0 selects 1/sqrt(head_dim).
  * Errors: PP_ERR_UNSUPPORTED for another head_dim; PP_ERR_INVALID_ARGUMENT for
  * null pointers or bad head counts; PP_ERR_BAD_LAYOUT for a bad descriptor;

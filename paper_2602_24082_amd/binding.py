@@ -68,7 +68,7 @@ def lib() -> ctypes.CDLL:
     i = ctypes.c_int
     sz = ctypes.c_size_t
     D = ctypes.POINTER(_Desc)
-    L.pp_workspace_size.argtypes = [D, i, i, i, i, ctypes.POINTER(sz), ctypes.POINTER(sz),
+    L.pp_workspace_size.argtypes = [D, i, i, i, i, i, ctypes.POINTER(sz), ctypes.POINTER(sz),
                                     ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.pp_attn_fwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, sz, P]
     L.pp_attn_bwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, P, P, P, P, sz, P]
@@ -140,13 +140,14 @@ def _workspace(nbytes: int, device) -> torch.Tensor:
 
 
 def pp_workspace_size(pack: Pack, hq: int = 1, hkv: int = 1, head_dim: int = 64, vocab: int = 0,
-                      fwd=True, bwd=True, logprob=False, loss=True):
-    """Workspace bytes (fwd, bwd, logprob, loss); entries not asked for are None."""
+                      fwd=True, bwd=True, logprob=False, loss=True, dtype: int = PP_BF16):
+    """Workspace bytes (fwd, bwd, logprob, loss); entries not asked for are None.
+    dtype is the attention input dtype code (PP_BF16 or PP_FP32)."""
     h = _DescHolder(pack)
     vals = [ctypes.c_size_t(0) for _ in range(4)]
     want = [fwd, bwd, logprob, loss]
     args = [ctypes.byref(v) if w else None for v, w in zip(vals, want)]
-    _check(lib().pp_workspace_size(h.ref, hq, hkv, head_dim, vocab, *args))
+    _check(lib().pp_workspace_size(h.ref, dtype, hq, hkv, head_dim, vocab, *args))
     return tuple(int(v.value) if w else None for v, w in zip(vals, want))
 
 
@@ -162,7 +163,7 @@ def pp_attn_fwd(pack: Pack, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, s
     if lse is None:
         lse = torch.empty(hq, T, dtype=torch.float32, device=q.device)
     if ws is None:
-        nb, = pp_workspace_size(pack, hq, hkv, d, fwd=True, bwd=False, loss=False)[:1]
+        nb, = pp_workspace_size(pack, hq, hkv, d, fwd=True, bwd=False, loss=False, dtype=_dtype_code(q))[:1]
         ws = _workspace(nb, q.device)
     _check(lib().pp_attn_fwd(h.ref, _dtype_code(q), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v),
                              _ptr(out), _ptr(lse), _ptr(ws), ws.numel(), _stream(q.device)))
@@ -179,7 +180,7 @@ def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, 
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
     if ws is None:
-        nb = pp_workspace_size(pack, hq, hkv, d, fwd=False, bwd=True, loss=False)[1]
+        nb = pp_workspace_size(pack, hq, hkv, d, fwd=False, bwd=True, loss=False, dtype=_dtype_code(q))[1]
         ws = _workspace(nb, q.device)
     _check(lib().pp_attn_bwd(h.ref, _dtype_code(q), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v),
                              _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),

@@ -4,20 +4,24 @@
 //
 //   bwd_prep   delta_i = dO_i . O_i  (fp32, [hq, sumT])
 //   bwd_dkdv   key-major: one workgroup = one 128-key tile of one kv-head, four
-//              waves of 32 keys.  It walks every query that sees the tile, for
-//              each query head of the kv-head's group, 32 queries per step.
-//              A prompt key tile is therefore visited by the prompt's later
-//              queries AND by every response's queries, so the shared prompt's
-//              dK/dV gather all K responses' contributions in one place.
-//              Per step (S = Q K^T orientation, lane = key):
+//              waves of 32 keys each (K, V and the dK, dV accumulators live in
+//              registers).  It walks every query that sees the tile, for each
+//              query head of the kv-head's group, 64 queries per step, with the
+//              Q and dO tiles DMA'd into a double-buffered LDS stage.  A prompt
+//              key tile is visited by the prompt's later queries AND by every
+//              response's queries, so the shared prompt's dK/dV gather all K
+//              responses' contributions in one place.  Per step (S = Q K^T,
+//              lane = key):
 //                P  = exp2(S*scale*log2e - lse_i*log2e) (masked)
 //                dP = dO V^T,  dS = P (dP - delta_i)
-//                dV^T += dO^T P,  dK^T += Q^T dS
+//                dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T by transposed LDS reads)
 //   bwd_dq     query-major, like the forward (lane = query):
 //                S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - delta)
 //                dQ^T += K^T dS^T
 //
-// All products run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
+// All products run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Q, K, V
+// and dO are bf16 here (fp32 callers are converted by a pre-pass); O and the
+// gradients use the caller's dtype.
 
 #include <hip/hip_runtime.h>
 
@@ -27,17 +31,18 @@
 namespace pp {
 namespace {
 
-template <typename T>
+template <typename TO>
 struct BwdParams {
-  const T* q;
-  const T* k;
-  const T* v;
-  const T* o;
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  const __bf16* dout;
+  const TO* o;       // caller dtype
+  const TO* dout_o;  // dO in the caller dtype (for delta)
   const float* lse;
-  const T* dout;
-  T* dq;
-  T* dk;
-  T* dv;
+  TO* dq;
+  TO* dk;
+  TO* dv;
   float* delta;
   const QTileItem* dq_items;
   const int32_t* dq_ktiles;
@@ -52,17 +57,17 @@ struct BwdParams {
 // delta = rowsum(dO * O)
 // ---------------------------------------------------------------------------
 
-template <int D, typename T>
-__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<T> p, int64_t n_rows) {
-  constexpr int LPR = D / 8;                 // lanes per (token, head) row
-  constexpr int RPB = 256 / LPR;             // rows per block
+template <int D, typename TO>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t n_rows) {
+  constexpr int LPR = D / 8;      // lanes per (token, head) row
+  constexpr int RPB = 256 / LPR;  // rows per block
   const int tid = threadIdx.x;
   const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;
   const int part = tid % LPR;
   float acc = 0.f;
   if (row < n_rows) {
-    const bf16x8 a = load8_bf16<T>(p.dout + row * D + part * 8);
-    const bf16x8 b = load8_bf16<T>(p.o + row * D + part * 8);
+    const TO* a = p.dout_o + row * D + part * 8;
+    const TO* b = p.o + row * D + part * 8;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc += (float)a[e] * (float)b[e];
   }
@@ -79,20 +84,19 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<T> p, int64_t n
 // ---------------------------------------------------------------------------
 
 constexpr int KBN = kBwdBlockN;  // 128 keys per workgroup
-constexpr int KBM = kBwdBlockM;  // 32 queries per step
+constexpr int KBM = kBwdBlockM;  // 64 queries per step
 
-template <int D, typename T>
-__global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams<T> p) {
-  constexpr int RS = D + 8;    // row-major stride (bf16)
-  constexpr int TS = KBM + 8;  // transposed stride
-  __shared__ __attribute__((aligned(16))) __bf16 sQ[KBM * RS];
-  __shared__ __attribute__((aligned(16))) __bf16 sdO[KBM * RS];
-  __shared__ __attribute__((aligned(16))) __bf16 sQt[D * TS];
-  __shared__ __attribute__((aligned(16))) __bf16 sdOt[D * TS];
-  __shared__ float sL[KBM];   // lse * log2(e)
-  __shared__ float sDl[KBM];  // delta
-  __shared__ int sHi[KBM];
-  __shared__ int sLo[KBM];
+struct QInfo {
+  float lse2;   // lse * log2(e)
+  float delta;
+  int hi;       // query index if real, else -1
+  int lo;       // start of the query's segment
+};
+
+template <int D, typename TO>
+__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
+  __shared__ __attribute__((aligned(1024))) __bf16 sQD[2][2][KBM * D];  // [stage][Q/dO]
+  __shared__ QInfo sInfo[2][KBM];
 
   const int item_idx = blockIdx.x / p.hkv;
   const int g = blockIdx.x % p.hkv;
@@ -111,16 +115,49 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams<T> p) {
   const bool k_real = j < it.valid;
   const int64_t krow = (int64_t)(it.tok0 + j) * p.hkv + g;
 
+  const int wk0 = it.k0 + wave * 32;
+  const int wk1 = min(min(it.k_end, it.valid), wk0 + 32);
+  const bool wave_live = wk0 < wk1;
+
+  const int nq = it.q_end - it.q_begin;
+  const int nsteps = (nq + KBM - 1) / KBM;
+  const int n_iter = nq > 0 ? G * nsteps : 0;
+  const int64_t q_stride = (int64_t)p.hq * D;
+
+  auto issue = [&](int n, int stage) {
+    const int hh = n / nsteps, st = n - hh * nsteps;
+    const int head = g * G + hh;
+    const int qs = it.q_begin + st * KBM;
+    const int rows = min(KBM, it.q_end - qs);
+    const __bf16* qb = p.q + ((int64_t)(it.tok0 + qs) * p.hq + head) * D;
+    const __bf16* db = p.dout + ((int64_t)(it.tok0 + qs) * p.hq + head) * D;
+    dma_rows<D, KBM / 4>(sQD[stage][0], qb, q_stride, wave * (KBM / 4), rows, lane);
+    dma_rows<D, KBM / 4>(sQD[stage][1], db, q_stride, wave * (KBM / 4), rows, lane);
+  };
+  auto load_info = [&](int n) -> QInfo {
+    const int hh = n / nsteps, st = n - hh * nsteps;
+    const int head = g * G + hh;
+    const int qi = it.q_begin + st * KBM + tid;
+    QInfo r;
+    const bool real = qi < it.q_end && qi < it.valid;
+    const int64_t tq = (int64_t)it.tok0 + qi;
+    r.lse2 = real ? p.lse[(int64_t)head * p.sumT + tq] * kLog2e : 0.f;
+    r.delta = real ? p.delta[(int64_t)head * p.sumT + tq] : 0.f;
+    r.hi = real ? qi : -1;
+    r.lo = real ? p.seg_lo[tq] : 0;
+    return r;
+  };
+
+  if (n_iter > 0) {
+    issue(0, 0);
+    if (tid < KBM) sInfo[0][tid] = load_info(0);
+  }
+
   bf16x8 kf[D / 16], vf[D / 16];
 #pragma unroll
   for (int c = 0; c < D / 16; ++c) {
-    if (k_real) {
-      kf[c] = load8_bf16<T>(p.k + krow * D + 16 * c + 8 * hf);
-      vf[c] = load8_bf16<T>(p.v + krow * D + 16 * c + 8 * hf);
-    } else {
-      kf[c] = bf16x8{};
-      vf[c] = bf16x8{};
-    }
+    kf[c] = k_real ? *reinterpret_cast<const bf16x8*>(p.k + krow * D + 16 * c + 8 * hf) : bf16x8{};
+    vf[c] = k_real ? *reinterpret_cast<const bf16x8*>(p.v + krow * D + 16 * c + 8 * hf) : bf16x8{};
   }
   f32x16 acc_dk[D / 32], acc_dv[D / 32];
 #pragma unroll
@@ -129,100 +166,60 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams<T> p) {
     acc_dv[m] = f32x16{};
   }
 
-  // wave's real keys [wk0, wk1)
-  const int wk0 = it.k0 + wave * 32;
-  const int wk1 = min(min(it.k_end, it.valid), wk0 + 32);
-  const bool wave_live = wk0 < wk1;
-
-  for (int hh = 0; hh < G; ++hh) {
-    const int head = g * G + hh;
-    for (int qs = it.q_begin; qs < it.q_end; qs += KBM) {
-      const int qe = min(qs + KBM, it.q_end);
-      __syncthreads();
-      // ---- stage Q, dO (row-major and transposed), lse, delta, hi, lo
-      for (int c = tid; c < 2 * (KBM / 4) * (D / 8); c += 256) {
-        const int which = c / ((KBM / 4) * (D / 8));  // 0: Q, 1: dO
-        const int rem = c % ((KBM / 4) * (D / 8));
-        const int grp = rem % (KBM / 4), col = rem / (KBM / 4);
-        const T* src = which ? p.dout : p.q;
-        __bf16* dst = which ? sdO : sQ;
-        __bf16* dstT = which ? sdOt : sQt;
-        bf16x8 rows[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int qi = qs + grp * 4 + r;
-          rows[r] = qi < qe ? load8_bf16<T>(src + ((int64_t)(it.tok0 + qi) * p.hq + head) * D + col * 8)
-                            : bf16x8{};
-          *reinterpret_cast<bf16x8*>(&dst[(grp * 4 + r) * RS + col * 8]) = rows[r];
-        }
-        const int pos = row_group_pos(grp);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          bf16x4 w = {rows[0][e], rows[1][e], rows[2][e], rows[3][e]};
-          *reinterpret_cast<bf16x4*>(&dstT[(col * 8 + e) * TS + pos]) = w;
-        }
-      }
-      if (tid < KBM) {
-        const int qi = qs + tid;
-        const bool real = qi < qe && qi < it.valid;
-        const int64_t tq = it.tok0 + qi;
-        sL[tid] = real ? p.lse[(int64_t)head * p.sumT + tq] * kLog2e : 0.f;
-        sDl[tid] = real ? p.delta[(int64_t)head * p.sumT + tq] : 0.f;
-        sHi[tid] = real ? qi : -1;
-        sLo[tid] = real ? p.seg_lo[tq] : 0;
-      }
-      __syncthreads();
-      if (!wave_live) continue;
-      // causal: every query of the step precedes every key of the wave
-      const int last_real_q = min(qe, it.valid) - 1;
-      if (last_real_q < wk0) continue;
-
-      // ---- S = Q K^T, dP = dO V^T (lane = key, registers = queries)
-      f32x16 s = f32x16{}, dp = f32x16{};
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sQ[ln * RS + 16 * c + 8 * hf]);
-        s = mfma32(a, kf[c], s);
-      }
-#pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sdO[ln * RS + 16 * c + 8 * hf]);
-        dp = mfma32(a, vf[c], dp);
-      }
-      // ---- P and dS
-      bool any = false;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int il = 8 * (r >> 2) + 4 * hf + (r & 3);
-        const int hi = sHi[il], lo = sLo[il];
-        const bool vis = j <= hi && (j < it.P || j >= lo);
-        const float pr = vis ? exp2f(fmaf(s[r], p.scale_log2, -sL[il])) : 0.f;
-        any = any || vis;
-        s[r] = pr;
-        dp[r] = pr * (dp[r] - sDl[il]);
-      }
-      if (!__any(any)) continue;
-      bf16x8 pb[2], db[2];
-      pb[0] = acc_half_to_bf16(s, 0);
-      pb[1] = acc_half_to_bf16(s, 1);
-      db[0] = acc_half_to_bf16(dp, 0);
-      db[1] = acc_half_to_bf16(dp, 1);
-      // ---- dV^T += dO^T P, dK^T += Q^T dS
-#pragma unroll
-      for (int m = 0; m < D / 32; ++m)
-#pragma unroll
-        for (int ch = 0; ch < 2; ++ch) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sdOt[(32 * m + ln) * TS + 16 * ch + 8 * hf]);
-          acc_dv[m] = mfma32(a, pb[ch], acc_dv[m]);
-          const bf16x8 b = *reinterpret_cast<const bf16x8*>(&sQt[(32 * m + ln) * TS + 16 * ch + 8 * hf]);
-          acc_dk[m] = mfma32(b, db[ch], acc_dk[m]);
-        }
+  for (int n = 0; n < n_iter; ++n) {
+    const int stage = n & 1;
+    wait_vmem_all();
+    __syncthreads();  // step n landed; stage n+1 free
+    QInfo nxt;
+    const bool more = n + 1 < n_iter;
+    if (more) {
+      issue(n + 1, stage ^ 1);
+      if (tid < KBM) nxt = load_info(n + 1);
     }
+    const int st = n % nsteps;
+    const int qs = it.q_begin + st * KBM;
+    if (wave_live) {
+      const __bf16* sQ = sQD[stage][0];
+      const __bf16* sdO = sQD[stage][1];
+      const QInfo* inf = sInfo[stage];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        // queries past the range sit at the end of a block; a block whose first
+        // query is not real, or whose last real query precedes every key of the
+        // wave, has no visible pair
+        if (inf[qb * 32].hi < 0) continue;
+        const int blk_last = min(qs + qb * 32 + 31, min(it.q_end, it.valid) - 1);
+        if (blk_last < wk0) continue;
+        f32x16 s = f32x16{}, dp = f32x16{};
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) s = mfma32(lds_row8<D>(sQ, qb * 32 + ln, 2 * c + hf), kf[c], s);
+#pragma unroll
+        for (int c = 0; c < D / 16; ++c) dp = mfma32(lds_row8<D>(sdO, qb * 32 + ln, 2 * c + hf), vf[c], dp);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const QInfo q = inf[qb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)];
+          const bool vis = j <= q.hi && (j < it.P || j >= q.lo);
+          const float pr = vis ? exp2f(fmaf(s[r], p.scale_log2, -q.lse2)) : 0.f;
+          s[r] = pr;
+          dp[r] = pr * (dp[r] - q.delta);
+        }
+        const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
+        const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
+#pragma unroll
+        for (int m = 0; m < D / 32; ++m) {
+          acc_dv[m] = mfma32(lds_tr8<D>(sdO, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
+          acc_dv[m] = mfma32(lds_tr8<D>(sdO, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
+          acc_dk[m] = mfma32(lds_tr8<D>(sQ, qb * 32, 32 * m, lane), db0, acc_dk[m]);
+          acc_dk[m] = mfma32(lds_tr8<D>(sQ, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
+        }
+      }
+    }
+    if (more && tid < KBM) sInfo[stage ^ 1][tid] = nxt;
   }
 
   if (!k_in_tile) return;
-  T* dkrow = p.dk + krow * D;
-  T* dvrow = p.dv + krow * D;
+  TO* dkrow = p.dk + krow * D;
+  TO* dvrow = p.dv + krow * D;
 #pragma unroll
   for (int m = 0; m < D / 32; ++m)
 #pragma unroll
@@ -231,8 +228,8 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams<T> p) {
       f32x4 kv = {acc_dk[m][4 * r4] * p.scale, acc_dk[m][4 * r4 + 1] * p.scale,
                   acc_dk[m][4 * r4 + 2] * p.scale, acc_dk[m][4 * r4 + 3] * p.scale};
       f32x4 vv = {acc_dv[m][4 * r4], acc_dv[m][4 * r4 + 1], acc_dv[m][4 * r4 + 2], acc_dv[m][4 * r4 + 3]};
-      store4<T>(dkrow + d0, kv);
-      store4<T>(dvrow + d0, vv);
+      store4<TO>(dkrow + d0, kv);
+      store4<TO>(dvrow + d0, vv);
     }
 }
 
@@ -243,13 +240,9 @@ __global__ __launch_bounds__(256) void bwd_dkdv_kernel(BwdParams<T> p) {
 constexpr int QBM = kDqBlockM;  // 128
 constexpr int QBN = kDqBlockN;  // 64
 
-template <int D, typename T>
-__global__ __launch_bounds__(256) void bwd_dq_kernel(BwdParams<T> p) {
-  constexpr int RS = D + 8;
-  constexpr int TS = QBN + 8;
-  __shared__ __attribute__((aligned(16))) __bf16 sK[QBN * RS];
-  __shared__ __attribute__((aligned(16))) __bf16 sV[QBN * RS];
-  __shared__ __attribute__((aligned(16))) __bf16 sKt[D * TS];
+template <int D, typename TO>
+__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
+  __shared__ __attribute__((aligned(1024))) __bf16 sKV[2][2][QBN * D];
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
@@ -269,62 +262,47 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdParams<T> p) {
   const int hi = real ? i : -1;
   const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
+
+  const int64_t kv_stride = (int64_t)p.hkv * D;
+  const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const int kv_lim = it.valid;
+  const int n_tiles = it.kt_cnt;
+
+  if (n_tiles > 0) {
+    const int k0 = p.dq_ktiles[it.kt_off];
+    const int rows = min(QBN, kv_lim - k0);
+    dma_rows<D, QBN / 4>(sKV[0][0], kbase + k0 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
+    dma_rows<D, QBN / 4>(sKV[0][1], vbase + k0 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
+  }
+
   const float lse2 = real ? p.lse[(int64_t)head * p.sumT + it.tok0 + i] * kLog2e : 0.f;
   const float dlt = real ? p.delta[(int64_t)head * p.sumT + it.tok0 + i] : 0.f;
-
   bf16x8 qf[D / 16], df[D / 16];
 #pragma unroll
   for (int c = 0; c < D / 16; ++c) {
-    if (in_tile) {
-      qf[c] = load8_bf16<T>(p.q + qrow * D + 16 * c + 8 * hf);
-      df[c] = load8_bf16<T>(p.dout + qrow * D + 16 * c + 8 * hf);
-    } else {
-      qf[c] = bf16x8{};
-      df[c] = bf16x8{};
-    }
+    qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
+    df[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.dout + qrow * D + 16 * c + 8 * hf) : bf16x8{};
   }
   f32x16 acc[D / 32];
 #pragma unroll
   for (int m = 0; m < D / 32; ++m) acc[m] = f32x16{};
 
-  const int wave_q0 = it.q0 + wave * 32;
-  const bool wave_live = wave_q0 < it.q_end;
-  const int kv_lim = it.valid;
+  const bool wave_live = it.q0 + wave * 32 < it.q_end;
 
-  for (int t = 0; t < it.kt_cnt; ++t) {
+  for (int t = 0; t < n_tiles; ++t) {
     const int k0 = p.dq_ktiles[it.kt_off + t];
+    wait_vmem_all();
     __syncthreads();
-    for (int c = tid; c < QBN * (D / 8); c += 256) {
-      const int r = c / (D / 8), col = c % (D / 8);
-      const int key = k0 + r;
-      bf16x8 kv = bf16x8{}, vv = bf16x8{};
-      if (key < kv_lim) {
-        const int64_t off = ((int64_t)(it.tok0 + key) * p.hkv + g) * D + col * 8;
-        kv = load8_bf16<T>(p.k + off);
-        vv = load8_bf16<T>(p.v + off);
-      }
-      *reinterpret_cast<bf16x8*>(&sK[r * RS + col * 8]) = kv;
-      *reinterpret_cast<bf16x8*>(&sV[r * RS + col * 8]) = vv;
+    if (t + 1 < n_tiles) {
+      const int k1 = p.dq_ktiles[it.kt_off + t + 1];
+      const int rows = min(QBN, kv_lim - k1);
+      dma_rows<D, QBN / 4>(sKV[(t + 1) & 1][0], kbase + k1 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
+      dma_rows<D, QBN / 4>(sKV[(t + 1) & 1][1], vbase + k1 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
     }
-    for (int c = tid; c < (QBN / 4) * (D / 8); c += 256) {
-      const int grp = c % (QBN / 4), col = c / (QBN / 4);
-      bf16x8 rows[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + grp * 4 + r;
-        rows[r] = key < kv_lim
-                      ? load8_bf16<T>(p.k + ((int64_t)(it.tok0 + key) * p.hkv + g) * D + col * 8)
-                      : bf16x8{};
-      }
-      const int pos = row_group_pos(grp);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16x4 w = {rows[0][e], rows[1][e], rows[2][e], rows[3][e]};
-        *reinterpret_cast<bf16x4*>(&sKt[(col * 8 + e) * TS + pos]) = w;
-      }
-    }
-    __syncthreads();
     if (!wave_live) continue;
+    const __bf16* sK = sKV[t & 1][0];
+    const __bf16* sV = sKV[t & 1][1];
 
     const int k_last = k0 + QBN - 1;
     const bool lane_any = in_tile && hi >= k0 && (k0 < it.P || max(k0, lo) <= min(hi, k_last));
@@ -338,15 +316,9 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdParams<T> p) {
       s[kb] = f32x16{};
       dp[kb] = f32x16{};
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[(kb * 32 + ln) * RS + 16 * c + 8 * hf]);
-        s[kb] = mfma32(a, qf[c], s[kb]);
-      }
+      for (int c = 0; c < D / 16; ++c) s[kb] = mfma32(lds_row8<D>(sK, kb * 32 + ln, 2 * c + hf), qf[c], s[kb]);
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sV[(kb * 32 + ln) * RS + 16 * c + 8 * hf]);
-        dp[kb] = mfma32(a, df[c], dp[kb]);
-      }
+      for (int c = 0; c < D / 16; ++c) dp[kb] = mfma32(lds_row8<D>(sV, kb * 32 + ln, 2 * c + hf), df[c], dp[kb]);
     }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -364,38 +336,36 @@ __global__ __launch_bounds__(256) void bwd_dq_kernel(BwdParams<T> p) {
       db[2 * kb + 1] = acc_half_to_bf16(dp[kb], 1);
     }
 #pragma unroll
-    for (int m = 0; m < D / 32; ++m)
+    for (int ch = 0; ch < 4; ++ch)
 #pragma unroll
-      for (int ch = 0; ch < 4; ++ch) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sKt[(32 * m + ln) * TS + 16 * ch + 8 * hf]);
-        acc[m] = mfma32(a, db[ch], acc[m]);
-      }
+      for (int m = 0; m < D / 32; ++m) acc[m] = mfma32(lds_tr8<D>(sK, 16 * ch, 32 * m, lane), db[ch], acc[m]);
   }
 
   if (!in_tile) return;
-  T* row = p.dq + qrow * D;
+  TO* row = p.dq + qrow * D;
 #pragma unroll
   for (int m = 0; m < D / 32; ++m)
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       f32x4 v4 = {acc[m][4 * r4] * p.scale, acc[m][4 * r4 + 1] * p.scale, acc[m][4 * r4 + 2] * p.scale,
                   acc[m][4 * r4 + 3] * p.scale};
-      store4<T>(row + 32 * m + 8 * r4 + 4 * hf, v4);
+      store4<TO>(row + 32 * m + 8 * r4 + 4 * hf, v4);
     }
 }
 
-template <int D, typename T>
+template <int D, typename TO>
 hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
-  BwdParams<T> p;
-  p.q = (const T*)a.q;
-  p.k = (const T*)a.k;
-  p.v = (const T*)a.v;
-  p.o = (const T*)a.o;
+  BwdParams<TO> p;
+  p.q = (const __bf16*)a.q;
+  p.k = (const __bf16*)a.k;
+  p.v = (const __bf16*)a.v;
+  p.dout = (const __bf16*)a.dout;
+  p.o = (const TO*)a.o;
+  p.dout_o = (const TO*)a.dout_orig;
   p.lse = a.lse;
-  p.dout = (const T*)a.dout;
-  p.dq = (T*)a.dq;
-  p.dk = (T*)a.dk;
-  p.dv = (T*)a.dv;
+  p.dq = (TO*)a.dq;
+  p.dk = (TO*)a.dk;
+  p.dv = (TO*)a.dv;
   p.delta = a.delta;
   p.dq_items = a.dq_items;
   p.dq_ktiles = a.dq_ktiles;
@@ -411,21 +381,21 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   {
     constexpr int RPB = 256 / (D / 8);
     TimingScope t("pp_attn_bwd_prep", s);
-    hipLaunchKernelGGL((bwd_prep_kernel<D, T>), dim3((unsigned)((n_rows + RPB - 1) / RPB)), dim3(256), 0, s,
+    hipLaunchKernelGGL((bwd_prep_kernel<D, TO>), dim3((unsigned)((n_rows + RPB - 1) / RPB)), dim3(256), 0, s,
                        p, n_rows);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dkdv", s);
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, T>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(256),
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(256),
                        0, s, p);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dq", s);
-    hipLaunchKernelGGL((bwd_dq_kernel<D, T>), dim3((unsigned)((int64_t)a.n_dq_items * a.hq)), dim3(256), 0,
+    hipLaunchKernelGGL((bwd_dq_kernel<D, TO>), dim3((unsigned)((int64_t)a.n_dq_items * a.hq)), dim3(256), 0,
                        s, p);
   }
   return hipGetLastError();
@@ -433,6 +403,7 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
 
 }  // namespace
 
+// q, k, v, dout are bf16 here; a.dtype is the dtype of o, dout_orig and the gradients.
 hipError_t launch_attn_bwd(const AttnBwdLaunch& a, hipStream_t s) {
   if (a.dtype == kBF16) {
     if (a.head_dim == 128) return launch_bwd_t<128, __bf16>(a, s);

@@ -6,16 +6,20 @@
 // the causal upper triangle and a response's view of its siblings -- are never
 // listed).  Per key tile:
 //
-//   * K is staged row-major in LDS and V transposed (d-major, keys permuted in
-//     groups of four to match the MFMA register layout of P);
+//   * K and V are DMA'd (global_load_lds) into a double-buffered, swizzled LDS
+//     stage while the previous tile is being computed: one barrier per tile;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: lane l owns query l%32, so the
 //     softmax row statistics stay in the lane (one cross-half exchange);
 //   * the mask is evaluated only when the tile is not fully visible to the
 //     wave: visible(i, j) = j <= hi_i && (j < P || j >= lo_i);
-//   * online softmax in base 2 with scale*log2(e) folded in;
-//   * O^T += V^T P^T, with P converted to bf16 straight from the accumulators.
+//   * base-2 online softmax with scale*log2(e) folded in; the running maximum
+//     is only raised when a tile exceeds it by more than 2^8, so most tiles
+//     skip the rescale of O;
+//   * O^T += V^T P^T: P goes from the accumulators to bf16 B operands, V^T is
+//     read with ds_read_b64_tr_b16 straight from the row-major V tile.
 //
-// Inputs in fp32 are rounded to bf16 when loaded; accumulation is fp32.
+// Q, K, V are bf16 (fp32 callers are converted by a pre-pass); O is written in
+// the caller's dtype.
 
 #include <hip/hip_runtime.h>
 
@@ -27,13 +31,14 @@ namespace {
 
 constexpr int BM = kFwdBlockM;  // 128
 constexpr int BN = kFwdBlockN;  // 64
+constexpr float kRescaleSlack = 8.0f;  // log2 units
 
-template <typename T>
+template <typename TO>
 struct FwdParams {
-  const T* q;
-  const T* k;
-  const T* v;
-  T* o;
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  TO* o;
   float* lse;
   const QTileItem* items;
   const int32_t* ktiles;
@@ -43,12 +48,9 @@ struct FwdParams {
   float scale_log2;
 };
 
-template <int D, typename T>
-__global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams<T> p) {
-  constexpr int KS = D + 8;   // LDS row stride of K (bf16 elements)
-  constexpr int VS = BN + 8;  // LDS row stride of V^T
-  __shared__ __attribute__((aligned(16))) __bf16 sK[BN * KS];
-  __shared__ __attribute__((aligned(16))) __bf16 sVt[D * VS];
+template <int D, typename TO>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
+  __shared__ __attribute__((aligned(1024))) __bf16 sKV[2][2][BN * D];  // [stage][K/V][row*D]
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
@@ -62,7 +64,6 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams<T> p) {
   const int ln = lane & 31;
   const int hf = lane >> 5;
 
-  // this lane's query
   const int i = it.q0 + wave * 32 + ln;
   const bool in_tile = i < it.q_end;
   const bool real = i < it.valid;
@@ -70,55 +71,48 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams<T> p) {
   const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
 
+  const int64_t kv_stride = (int64_t)p.hkv * D;
+  const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const int kv_lim = it.valid;
+  const int n_tiles = it.kt_cnt;
+
+  // prologue: first key tile in flight before Q is read
+  if (n_tiles > 0) {
+    const int k0 = p.ktiles[it.kt_off];
+    const int rows = min(BN, kv_lim - k0);
+    dma_rows<D, BN / 4>(sKV[0][0], kbase + k0 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
+    dma_rows<D, BN / 4>(sKV[0][1], vbase + k0 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
+  }
+
   bf16x8 qf[D / 16];
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    if (in_tile) qf[c] = load8_bf16<T>(p.q + qrow * D + 16 * c + 8 * hf);
-    else qf[c] = bf16x8{};
-  }
+  for (int c = 0; c < D / 16; ++c)
+    qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
 
   f32x16 acc_o[D / 32];
 #pragma unroll
   for (int m = 0; m < D / 32; ++m) acc_o[m] = f32x16{};
-  float m_run = kNegInf;  // running max of raw scores
+  float m_ref = kNegInf;  // reference maximum, scaled log2 units
   float l_run = 0.f;      // this lane's partial softmax denominator
 
-  const int wave_q0 = it.q0 + wave * 32;
-  const bool wave_live = wave_q0 < it.q_end;
-  const int kv_lim = it.valid;  // keys at or past this are padding or another row
+  const bool wave_live = it.q0 + wave * 32 < it.q_end;
+  const float c2 = p.scale_log2;
 
-  for (int t = 0; t < it.kt_cnt; ++t) {
+  for (int t = 0; t < n_tiles; ++t) {
     const int k0 = p.ktiles[it.kt_off + t];
-    __syncthreads();
-    // ---- stage K (row-major) and V^T (d-major, permuted key groups) in LDS
-    for (int c = tid; c < BN * (D / 8); c += 256) {
-      const int r = c / (D / 8), col = c % (D / 8);
-      const int key = k0 + r;
-      bf16x8 val = bf16x8{};
-      if (key < kv_lim) val = load8_bf16<T>(p.k + ((int64_t)(it.tok0 + key) * p.hkv + g) * D + col * 8);
-      *reinterpret_cast<bf16x8*>(&sK[r * KS + col * 8]) = val;
+    wait_vmem_all();
+    __syncthreads();  // tile t landed for every wave; stage (t+1)&1 is free
+    if (t + 1 < n_tiles) {
+      const int k1 = p.ktiles[it.kt_off + t + 1];
+      const int rows = min(BN, kv_lim - k1);
+      dma_rows<D, BN / 4>(sKV[(t + 1) & 1][0], kbase + k1 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
+      dma_rows<D, BN / 4>(sKV[(t + 1) & 1][1], vbase + k1 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
     }
-    for (int c = tid; c < (BN / 4) * (D / 8); c += 256) {
-      const int grp = c % (BN / 4), col = c / (BN / 4);
-      bf16x8 rows[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + grp * 4 + r;
-        rows[r] = key < kv_lim
-                      ? load8_bf16<T>(p.v + ((int64_t)(it.tok0 + key) * p.hkv + g) * D + col * 8)
-                      : bf16x8{};
-      }
-      const int pos = row_group_pos(grp);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        bf16x4 w = {rows[0][e], rows[1][e], rows[2][e], rows[3][e]};
-        *reinterpret_cast<bf16x4*>(&sVt[(col * 8 + e) * VS + pos]) = w;
-      }
-    }
-    __syncthreads();
     if (!wave_live) continue;
+    const __bf16* sK = sKV[t & 1][0];
+    const __bf16* sV = sKV[t & 1][1];
 
-    // ---- does this key tile touch the wave's queries, and is it fully visible?
     const int k_last = k0 + BN - 1;
     const bool lane_any = in_tile && hi >= k0 && (k0 < it.P || max(k0, lo) <= min(hi, k_last));
     const bool lane_all = !in_tile || (k_last <= hi && (k0 + BN <= it.P || k0 >= lo));
@@ -131,10 +125,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams<T> p) {
     for (int kb = 0; kb < 2; ++kb) {
       s[kb] = f32x16{};
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sK[(kb * 32 + ln) * KS + 16 * c + 8 * hf]);
-        s[kb] = mfma32(a, qf[c], s[kb]);
-      }
+      for (int c = 0; c < D / 16; ++c) s[kb] = mfma32(lds_row8<D>(sK, kb * 32 + ln, 2 * c + hf), qf[c], s[kb]);
     }
     if (need_mask) {
 #pragma unroll
@@ -146,33 +137,37 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams<T> p) {
           s[kb][r] = vis ? s[kb][r] : kNegInf;
         }
     }
-    // ---- online softmax (row = this lane's query; the other half-wave holds
-    //      the remaining keys of the tile)
+    // ---- online softmax with a lazily raised reference maximum
     float mx = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == kNegInf) ? 0.f : m_new;
-    const float ms = m_use * p.scale_log2;
-    const float alpha = exp2f(m_run * p.scale_log2 - ms);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+    const bool raise = mx > m_ref + kRescaleSlack;
+    if (__any(raise)) {
+      const float m_new = raise ? mx : m_ref;
+      // a lane that has seen no visible key yet has O = 0 and l = 0 (its m_ref
+      // is -inf, and m_new may be -inf too): scale by 0 rather than exp2(nan)
+      const float alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc_o[m][r] *= alpha;
+      m_ref = m_new;
+    }
+    const float mref = (m_ref == kNegInf) ? 0.f : m_ref;
     float psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(fmaf(s[kb][r], p.scale_log2, -ms));
+        const float e = exp2f(fmaf(s[kb][r], c2, -mref));
         s[kb][r] = e;
         psum += e;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int m = 0; m < D / 32; ++m)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc_o[m][r] *= alpha;
+    l_run += psum;
 
     // ---- O^T += V^T P^T over four 16-key chunks
     bf16x8 pb[4];
@@ -182,36 +177,46 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(FwdParams<T> p) {
       pb[2 * kb + 1] = acc_half_to_bf16(s[kb], 1);
     }
 #pragma unroll
-    for (int m = 0; m < D / 32; ++m)
+    for (int ch = 0; ch < 4; ++ch)
 #pragma unroll
-      for (int ch = 0; ch < 4; ++ch) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&sVt[(32 * m + ln) * VS + 16 * ch + 8 * hf]);
-        acc_o[m] = mfma32(a, pb[ch], acc_o[m]);
-      }
+      for (int m = 0; m < D / 32; ++m) acc_o[m] = mfma32(lds_tr8<D>(sV, 16 * ch, 32 * m, lane), pb[ch], acc_o[m]);
   }
 
   if (!in_tile) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  T* orow = p.o + qrow * D;
+  TO* orow = p.o + qrow * D;
 #pragma unroll
   for (int m = 0; m < D / 32; ++m)
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       f32x4 v4 = {acc_o[m][4 * r4] * inv, acc_o[m][4 * r4 + 1] * inv, acc_o[m][4 * r4 + 2] * inv,
                   acc_o[m][4 * r4 + 3] * inv};
-      store4<T>(orow + 32 * m + 8 * r4 + 4 * hf, v4);
+      store4<TO>(orow + 32 * m + 8 * r4 + 4 * hf, v4);
     }
-  if (hf == 0) p.lse[(int64_t)head * p.sumT + it.tok0 + i] = l_tot > 0.f ? m_run * p.scale + logf(l_tot) : 0.f;
+  // ln sum_j exp(scale s_j) = (m_ref + log2 l) / log2(e)
+  if (hf == 0)
+    p.lse[(int64_t)head * p.sumT + it.tok0 + i] = l_tot > 0.f ? (m_ref + __log2f(l_tot)) * (1.0f / kLog2e) : 0.f;
 }
 
-template <int D, typename T>
+__global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ src, __bf16* __restrict__ dst,
+                                                      int64_t n) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i + 4 <= n) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(src + i);
+    *reinterpret_cast<bf16x4*>(dst + i) = __builtin_convertvector(v, bf16x4);
+  } else {
+    for (int64_t j = i; j < n; ++j) dst[j] = (__bf16)src[j];
+  }
+}
+
+template <int D, typename TO>
 hipError_t launch_fwd_t(const AttnFwdLaunch& a, hipStream_t s) {
-  FwdParams<T> p;
-  p.q = (const T*)a.q;
-  p.k = (const T*)a.k;
-  p.v = (const T*)a.v;
-  p.o = (T*)a.o;
+  FwdParams<TO> p;
+  p.q = (const __bf16*)a.q;
+  p.k = (const __bf16*)a.k;
+  p.v = (const __bf16*)a.v;
+  p.o = (TO*)a.o;
   p.lse = a.lse;
   p.items = a.items;
   p.ktiles = a.ktiles;
@@ -224,12 +229,21 @@ hipError_t launch_fwd_t(const AttnFwdLaunch& a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.n_items * a.hq;
   if (blocks == 0) return hipSuccess;
   TimingScope t("pp_attn_fwd", s);
-  hipLaunchKernelGGL((attn_fwd_kernel<D, T>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, TO>), dim3((unsigned)blocks), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
+hipError_t launch_to_bf16(const float* src, void* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  TimingScope t("pp_to_bf16", s);
+  const int64_t threads = (n + 3) / 4;
+  hipLaunchKernelGGL(to_bf16_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, src, (__bf16*)dst, n);
+  return hipGetLastError();
+}
+
+// q, k, v are bf16 here; a.dtype is the dtype of o.
 hipError_t launch_attn_fwd(const AttnFwdLaunch& a, hipStream_t s) {
   if (a.dtype == kBF16) {
     if (a.head_dim == 128) return launch_fwd_t<128, __bf16>(a, s);

@@ -88,6 +88,82 @@ __device__ __forceinline__ int row_group_pos(int group) {
   return (group >> 2) * 16 + p;
 }
 
+// ---------------------------------------------------------------------------
+// LDS tiles: [rows][D] bf16, rows packed back to back (D*2 bytes), with the
+// 16-byte chunks of row r XOR-swizzled by swz<D>(r).  The swizzle is a bijection
+// on every aligned group of 16 rows, so 16-byte reads of one logical chunk down
+// 16 consecutive rows hit 16 different bank groups; and the four rows x four
+// chunks that a half-wave touches in a transposed read also land in distinct
+// bank groups.  Tiles are filled by global_load_lds_dwordx4 (lane l of a wave
+// writes 16 bytes at the wave's LDS base + 16*l), so each lane fetches the
+// global chunk that belongs at its swizzled position.
+// ---------------------------------------------------------------------------
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+// Wave-cooperative DMA of rows [row0, row0 + NR) of a tile into LDS.  Row r of
+// the tile comes from `src + min(r, rows_valid - 1) * stride` (elements), so rows
+// past the valid range repeat the last valid row (finite data that the mask
+// then ignores).  NR * D * 2 must be a multiple of 1 KB.
+template <int D, int NR>
+__device__ __forceinline__ void dma_rows(__bf16* lds_tile, const __bf16* src, int64_t stride, int row0,
+                                         int rows_valid, int lane) {
+  constexpr int RPI = 1024 / (D * 2);  // rows per wave instruction
+  constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static_assert(NR % RPI == 0, "tile rows must fill whole wave loads");
+#pragma unroll
+  for (int i = 0; i < NR / RPI; ++i) {
+    const int rb = row0 + i * RPI;
+    const int r = rb + lane / CPR;
+    const int pc = lane % CPR;
+    const int lc = pc ^ swz<D>(r);
+    const int rs = min(r, rows_valid - 1);
+    __builtin_amdgcn_global_load_lds((const void*)(src + rs * stride + lc * 8),
+                                     (lds_void*)(lds_tile + rb * D), 16, 0, 0);
+  }
+}
+
+// 16-byte read of logical chunk `lc` (elements 8*lc .. 8*lc+7) of tile row r.
+template <int D>
+__device__ __forceinline__ bf16x8 lds_row8(const __bf16* tile, int r, int lc) {
+  return *reinterpret_cast<const bf16x8*>(tile + r * D + ((lc ^ swz<D>(r)) << 3));
+}
+
+// A operand of a 32x32x16 MFMA whose A[m][k] = tile[row(k)][col0 + m], i.e. the
+// tile read transposed: m runs along the row (d) axis, k along tile rows.  The
+// contraction index kk = 8h + e (h = lane/32) stands for tile row
+// row16 + perm16(kk): rows row16 + 4h + 0..3 for e < 4 and row16 + 8 + 4h + 0..3
+// for e >= 4, which is the order in which a 32x32 accumulator's registers hold
+// their rows (see acc_half_to_bf16).  Two ds_read_b64_tr_b16: in each group of
+// 16 lanes, lane 4r+q addresses 4 consecutive columns of row r and the hardware
+// returns to lane i the column i of the 4 rows.
+template <int D>
+__device__ __forceinline__ bf16x8 lds_tr8(const __bf16* tile, int row16, int col0, int lane) {
+  const int g = lane >> 4, a = lane & 15;
+  const int r = a >> 2, q = a & 3;
+  const int h = g >> 1;
+  const int col = col0 + 16 * (g & 1) + 4 * q;
+  const int lc = col >> 3, sub = col & 7;
+  const int r0 = row16 + 4 * h + r;
+  const int r1 = r0 + 8;
+  const __bf16* p0 = tile + r0 * D + ((lc ^ swz<D>(r0)) << 3) + sub;
+  const __bf16* p1 = tile + r1 * D + ((lc ^ swz<D>(r1)) << 3) + sub;
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p0);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p1);
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0); }
+
 __device__ __forceinline__ float wave_max(float x) {
   for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
   return x;

@@ -418,14 +418,21 @@ struct MetaImage {
 // Attention plan + layout
 // ---------------------------------------------------------------------------
 
+// bf16 copies of fp32 attention inputs live in the workspace after the plan.
+struct CastRegions {
+  bool on = false;
+  size_t q = 0, k = 0, v = 0, dout = 0;
+};
+
 struct FwdPlan {
   QPlan q;
   std::vector<int32_t> seg_lo;
   Layout lay;
   size_t r_seg, r_items, r_kt;
+  CastRegions cast;
 };
 
-void plan_fwd(const Batch& bt, FwdPlan* p) {
+void plan_fwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, FwdPlan* p) {
   build_qplan(bt, kFwdBlockM, kFwdBlockN, &p->q);
   build_seg_lo(bt, &p->seg_lo);
   p->lay = Layout();
@@ -433,6 +440,12 @@ void plan_fwd(const Batch& bt, FwdPlan* p) {
   p->r_items = p->lay.add(p->q.items.size() * sizeof(QTileItem));
   p->r_kt = p->lay.add(p->q.ktiles.size() * 4);
   p->lay.meta_bytes = p->lay.total;
+  if (dtype == PP_FP32) {
+    p->cast.on = true;
+    p->cast.q = p->lay.add((size_t)bt.sumT * hq * d * 2);
+    p->cast.k = p->lay.add((size_t)bt.sumT * hkv * d * 2);
+    p->cast.v = p->lay.add((size_t)bt.sumT * hkv * d * 2);
+  }
 }
 
 struct BwdPlan {
@@ -441,9 +454,10 @@ struct BwdPlan {
   std::vector<int32_t> seg_lo;
   Layout lay;
   size_t r_seg, r_dq_items, r_dq_kt, r_kv_items, r_delta;
+  CastRegions cast;
 };
 
-void plan_bwd(const Batch& bt, int hq, BwdPlan* p) {
+void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* p) {
   build_qplan(bt, kDqBlockM, kDqBlockN, &p->dq);
   build_kplan(bt, kBwdBlockN, &p->kv);
   build_seg_lo(bt, &p->seg_lo);
@@ -454,6 +468,13 @@ void plan_bwd(const Batch& bt, int hq, BwdPlan* p) {
   p->r_kv_items = p->lay.add(p->kv.size() * sizeof(KTileItem));
   p->lay.meta_bytes = p->lay.total;
   p->r_delta = p->lay.add((size_t)hq * bt.sumT * 4);
+  if (dtype == PP_FP32) {
+    p->cast.on = true;
+    p->cast.q = p->lay.add((size_t)bt.sumT * hq * d * 2);
+    p->cast.k = p->lay.add((size_t)bt.sumT * hkv * d * 2);
+    p->cast.v = p->lay.add((size_t)bt.sumT * hkv * d * 2);
+    p->cast.dout = p->lay.add((size_t)bt.sumT * hq * d * 2);
+  }
 }
 
 struct LogprobPlan {
@@ -582,23 +603,24 @@ const char* pp_status_string(pp_status s) {
 
 const char* pp_last_error(void) { return g_last_error.c_str(); }
 
-pp_status pp_workspace_size(const pp_pack_desc* desc, int hq, int hkv, int head_dim, int vocab,
-                            size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss) {
+pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                            int vocab, size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss) {
   Batch bt;
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (fwd || bwd) {
     st = check_heads(hq, hkv, head_dim);
     if (st != PP_OK) return st;
   }
   if (fwd) {
     FwdPlan p;
-    plan_fwd(bt, &p);
+    plan_fwd(bt, dtype, hq, hkv, head_dim, &p);
     *fwd = p.lay.total;
   }
   if (bwd) {
     BwdPlan p;
-    plan_bwd(bt, hq, &p);
+    plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
     *bwd = p.lay.total;
   }
   if (logprob) {
@@ -624,7 +646,7 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
   FwdPlan p;
-  plan_fwd(bt, &p);
+  plan_fwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lay.total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "forward needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
@@ -636,6 +658,20 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   img.put(p.lay.regions[p.r_items], p.q.items.data(), p.q.items.size() * sizeof(QTileItem));
   img.put(p.lay.regions[p.r_kt], p.q.ktiles.data(), p.q.ktiles.size() * 4);
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  hipError_t e;
+  if (p.cast.on) {
+    // the kernels read bf16: round fp32 inputs once (nearest even)
+    void* qb = at(ws, p.lay, p.cast.q);
+    void* kb = at(ws, p.lay, p.cast.k);
+    void* vb = at(ws, p.lay, p.cast.v);
+    if ((e = launch_to_bf16((const float*)q, qb, (int64_t)bt.sumT * hq * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)k, kb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)v, vb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess)
+      return hip_fail(e, "fp32 to bf16 conversion launch");
+    q = qb;
+    k = kb;
+    v = vb;
+  }
   AttnFwdLaunch a{};
   a.q = q;
   a.k = k;
@@ -652,7 +688,7 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   a.sumT = bt.sumT;
   a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
   a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
-  hipError_t e = launch_attn_fwd(a, s);
+  e = launch_attn_fwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention forward launch");
   return PP_OK;
 }
@@ -669,7 +705,7 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
   BwdPlan p;
-  plan_bwd(bt, hq, &p);
+  plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lay.total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
@@ -682,13 +718,31 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * 4);
   img.put(p.lay.regions[p.r_kv_items], p.kv.data(), p.kv.size() * sizeof(KTileItem));
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  hipError_t e;
+  const void* dout_bf = dout;
+  if (p.cast.on) {
+    void* qb = at(ws, p.lay, p.cast.q);
+    void* kb = at(ws, p.lay, p.cast.k);
+    void* vb = at(ws, p.lay, p.cast.v);
+    void* db = at(ws, p.lay, p.cast.dout);
+    if ((e = launch_to_bf16((const float*)q, qb, (int64_t)bt.sumT * hq * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)k, kb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)v, vb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)dout, db, (int64_t)bt.sumT * hq * head_dim, s)) != hipSuccess)
+      return hip_fail(e, "fp32 to bf16 conversion launch");
+    q = qb;
+    k = kb;
+    v = vb;
+    dout_bf = db;
+  }
   AttnBwdLaunch a{};
   a.q = q;
   a.k = k;
   a.v = v;
   a.o = o;
   a.lse = lse;
-  a.dout = dout;
+  a.dout = dout_bf;
+  a.dout_orig = dout;
   a.dq = dq;
   a.dk = dk;
   a.dv = dv;
@@ -705,7 +759,7 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   a.sumT = bt.sumT;
   a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
   a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
-  hipError_t e = launch_attn_bwd(a, s);
+  e = launch_attn_bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention backward launch");
   return PP_OK;
 }

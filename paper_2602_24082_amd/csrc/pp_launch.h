@@ -23,6 +23,10 @@ struct TimingScope {
   hipStream_t stream_;
 };
 
+// fp32 -> bf16 (round to nearest even) copy, for fp32 callers of attention.
+hipError_t launch_to_bf16(const float* src, void* dst, int64_t n, hipStream_t s);
+
+// q, k, v are bf16; o has dtype `dtype`.
 struct AttnFwdLaunch {
   const void* q;
   const void* k;
@@ -40,6 +44,7 @@ struct AttnFwdLaunch {
 };
 hipError_t launch_attn_fwd(const AttnFwdLaunch& a, hipStream_t s);
 
+// q, k, v, dout are bf16; o, dout_orig and the gradients have dtype `dtype`.
 struct AttnBwdLaunch {
   const void* q;
   const void* k;
@@ -47,6 +52,7 @@ struct AttnBwdLaunch {
   const void* o;
   const float* lse;
   const void* dout;
+  const void* dout_orig;
   void* dq;
   void* dk;
   void* dv;

@@ -25,7 +25,7 @@ constexpr int kFwdBlockN = 64;    // keys per forward k-tile
 constexpr int kDqBlockM = 128;    // queries per dQ workgroup
 constexpr int kDqBlockN = 64;     // keys per dQ k-tile
 constexpr int kBwdBlockN = 128;   // keys per dK/dV workgroup (4 waves x 32)
-constexpr int kBwdBlockM = 32;    // queries per dK/dV inner step
+constexpr int kBwdBlockM = 64;    // queries per dK/dV inner step
 
 // One query tile: queries [q0, q_end) of the row starting at flat index tok0.
 struct QTileItem {
