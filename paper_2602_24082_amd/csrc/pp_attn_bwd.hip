@@ -198,8 +198,9 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const QInfo q = inf[qb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)];
-          const bool vis = j <= q.hi && (j < it.P || j >= q.lo);
-          const float pr = vis ? exp2f(fmaf(s[r], p.scale_log2, -q.lse2)) : 0.f;
+          const bool vis = (j <= q.hi) & ((j < it.P) | (j >= q.lo));
+          const float e = fast_exp2(fmaf(s[r], p.scale_log2, -q.lse2));
+          const float pr = vis ? e : 0.f;
           s[r] = pr;
           dp[r] = pr * (dp[r] - q.delta);
         }
@@ -325,8 +326,9 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = k0 + kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-        const bool vis = !need_mask || (jj <= hi && (jj < it.P || jj >= lo));
-        const float pr = vis ? exp2f(fmaf(s[kb][r], p.scale_log2, -lse2)) : 0.f;
+        const bool vis = (!need_mask) | ((jj <= hi) & ((jj < it.P) | (jj >= lo)));
+        const float e = fast_exp2(fmaf(s[kb][r], p.scale_log2, -lse2));
+        const float pr = vis ? e : 0.f;
         dp[kb][r] = pr * (dp[kb][r] - dlt);
       }
     bf16x8 db[4];

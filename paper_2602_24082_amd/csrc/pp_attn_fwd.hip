@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int j = k0 + kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-          const bool vis = j <= hi && (j < it.P || j >= lo);
+          const bool vis = (j <= hi) & ((j < it.P) | (j >= lo));
           s[kb][r] = vis ? s[kb][r] : kNegInf;
         }
     }
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
       const float m_new = raise ? mx : m_ref;
       // a lane that has seen no visible key yet has O = 0 and l = 0 (its m_ref
       // is -inf, and m_new may be -inf too): scale by 0 rather than exp2(nan)
-      const float alpha = (m_ref == kNegInf) ? 0.f : exp2f(m_ref - m_new);
+      const float alpha = (m_ref == kNegInf) ? 0.f : fast_exp2(m_ref - m_new);
       l_run *= alpha;
 #pragma unroll
       for (int m = 0; m < D / 32; ++m)
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(fmaf(s[kb][r], c2, -mref));
+        const float e = fast_exp2(fmaf(s[kb][r], c2, -mref));
         s[kb][r] = e;
         psum += e;
       }

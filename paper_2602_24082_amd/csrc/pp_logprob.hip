@@ -43,7 +43,7 @@ struct MaxSum {
 __device__ __forceinline__ MaxSum combine(MaxSum a, MaxSum b) {
   const float m = fmaxf(a.m, b.m);
   if (m == kNegInf) return {kNegInf, 0.f};
-  const float s = a.s * exp2f((a.m - m) * kLog2e) + b.s * exp2f((b.m - m) * kLog2e);
+  const float s = a.s * fast_exp2((a.m - m) * kLog2e) + b.s * fast_exp2((b.m - m) * kLog2e);
   return {m, s};
 }
 
@@ -120,13 +120,13 @@ __global__ __launch_bounds__(kLpThreads) void logprob_rows_kernel(
       const float m = fmaxf(acc.m, mloc);
       if (m != kNegInf) {
         const float ml = m * kLog2e;
-        float s = acc.s * exp2f(acc.m * kLog2e - ml);
+        float s = acc.s * fast_exp2(acc.m * kLog2e - ml);
 #pragma unroll
         for (int j = 0; j < kLpUnroll; ++j) {
           const int vi = base + j * kLpThreads + tid;
           if (vi < nvec) {
 #pragma unroll
-            for (int e = 0; e < N; ++e) s += exp2f(fmaf(f[j * N + e], kLog2e, -ml));
+            for (int e = 0; e < N; ++e) s += fast_exp2(fmaf(f[j * N + e], kLog2e, -ml));
           }
         }
         acc = {m, s};
