@@ -7,7 +7,8 @@
 //              waves of 32 keys each (K, V and the dK, dV accumulators live in
 //              registers).  It walks every query that sees the tile, for each
 //              query head of the kv-head's group, 64 queries per step, with the
-//              Q and dO tiles DMA'd into a double-buffered LDS stage.  A prompt
+//              Q and dO tiles and the per-query LSE, delta and segment start
+//              DMA'd into a ring of LDS stages.  A prompt
 //              key tile is visited by the prompt's later queries AND by every
 //              response's queries, so the shared prompt's dK/dV gather all K
 //              responses' contributions in one place.  Per step (S = Q K^T,
@@ -86,17 +87,23 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t 
 constexpr int KBN = kBwdBlockN;  // 128 keys per workgroup
 constexpr int KBM = kBwdBlockM;  // 64 queries per step
 
-struct QInfo {
-  float lse2;   // lse * log2(e)
-  float delta;
-  int hi;       // query index if real, else -1
-  int lo;       // start of the query's segment
+// One pipeline stage of the dK/dV kernel: the step's Q and dO tiles and the
+// per-query scalars, all filled by DMA.
+template <int D>
+struct DkdvStage {
+  __bf16 q[KBM * D];
+  __bf16 dout[KBM * D];
+  float lse[KBM];
+  float delta[KBM];
+  int seg_lo[KBM];
+  int spare[KBM];  // receives the fourth wave's info DMA (keeps per-wave counts equal)
 };
 
-template <int D, typename TO>
+template <int D, int NS, typename TO>
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
-  __shared__ __attribute__((aligned(1024))) __bf16 sQD[2][2][KBM * D];  // [stage][Q/dO]
-  __shared__ QInfo sInfo[2][KBM];
+  using Dma = TileDma<D, KBM / 4>;
+  constexpr int PER_STEP = 2 * Dma::N + 1;  // DMA instructions per wave per step
+  __shared__ __attribute__((aligned(1024))) DkdvStage<D> st[NS];
 
   const int item_idx = blockIdx.x / p.hkv;
   const int g = blockIdx.x % p.hkv;
@@ -114,44 +121,17 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   const bool k_in_tile = j < it.k_end;
   const bool k_real = j < it.valid;
   const int64_t krow = (int64_t)(it.tok0 + j) * p.hkv + g;
+  const unsigned jP = (unsigned)(j - it.P);
 
   const int wk0 = it.k0 + wave * 32;
   const int wk1 = min(min(it.k_end, it.valid), wk0 + 32);
   const bool wave_live = wk0 < wk1;
+  const int qlim = min(it.q_end, it.valid);  // queries at or past this are not real
 
   const int nq = it.q_end - it.q_begin;
   const int nsteps = (nq + KBM - 1) / KBM;
   const int n_iter = nq > 0 ? G * nsteps : 0;
   const int64_t q_stride = (int64_t)p.hq * D;
-
-  auto issue = [&](int n, int stage) {
-    const int hh = n / nsteps, st = n - hh * nsteps;
-    const int head = g * G + hh;
-    const int qs = it.q_begin + st * KBM;
-    const int rows = min(KBM, it.q_end - qs);
-    const __bf16* qb = p.q + ((int64_t)(it.tok0 + qs) * p.hq + head) * D;
-    const __bf16* db = p.dout + ((int64_t)(it.tok0 + qs) * p.hq + head) * D;
-    dma_rows<D, KBM / 4>(sQD[stage][0], qb, q_stride, wave * (KBM / 4), rows, lane);
-    dma_rows<D, KBM / 4>(sQD[stage][1], db, q_stride, wave * (KBM / 4), rows, lane);
-  };
-  auto load_info = [&](int n) -> QInfo {
-    const int hh = n / nsteps, st = n - hh * nsteps;
-    const int head = g * G + hh;
-    const int qi = it.q_begin + st * KBM + tid;
-    QInfo r;
-    const bool real = qi < it.q_end && qi < it.valid;
-    const int64_t tq = (int64_t)it.tok0 + qi;
-    r.lse2 = real ? p.lse[(int64_t)head * p.sumT + tq] * kLog2e : 0.f;
-    r.delta = real ? p.delta[(int64_t)head * p.sumT + tq] : 0.f;
-    r.hi = real ? qi : -1;
-    r.lo = real ? p.seg_lo[tq] : 0;
-    return r;
-  };
-
-  if (n_iter > 0) {
-    issue(0, 0);
-    if (tid < KBM) sInfo[0][tid] = load_info(0);
-  }
 
   bf16x8 kf[D / 16], vf[D / 16];
 #pragma unroll
@@ -159,6 +139,28 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     kf[c] = k_real ? *reinterpret_cast<const bf16x8*>(p.k + krow * D + 16 * c + 8 * hf) : bf16x8{};
     vf[c] = k_real ? *reinterpret_cast<const bf16x8*>(p.v + krow * D + 16 * c + 8 * hf) : bf16x8{};
   }
+
+  Dma dma;
+  dma.init(wave * (KBM / 4), q_stride, lane);
+  auto issue = [&](int n) {
+    DkdvStage<D>& sg = st[n % NS];
+    const int hh = n / nsteps, stp = n - hh * nsteps;
+    const int head = g * G + hh;
+    const int qs = it.q_begin + stp * KBM;
+    const int rows = min(KBM, it.q_end - qs);
+    const int64_t t0 = (int64_t)it.tok0 + qs;
+    dma.issue(sg.q, p.q + (t0 * p.hq + head) * D, rows);
+    dma.issue(sg.dout, p.dout + (t0 * p.hq + head) * D, rows);
+    const int64_t tq = t0 + min(lane, rows - 1);
+    if (wave == 0) dma_dword(sg.lse, p.lse + (int64_t)head * p.sumT + tq);
+    else if (wave == 1) dma_dword(sg.delta, p.delta + (int64_t)head * p.sumT + tq);
+    else if (wave == 2) dma_dword(sg.seg_lo, p.seg_lo + tq);
+    else dma_dword(sg.spare, p.seg_lo + tq);
+  };
+#pragma unroll
+  for (int n = 0; n < NS - 1; ++n)
+    if (n < n_iter) issue(n);
+
   f32x16 acc_dk[D / 32], acc_dv[D / 32];
 #pragma unroll
   for (int m = 0; m < D / 32; ++m) {
@@ -167,55 +169,71 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   }
 
   for (int n = 0; n < n_iter; ++n) {
-    const int stage = n & 1;
-    wait_vmem_all();
-    __syncthreads();  // step n landed; stage n+1 free
-    QInfo nxt;
-    const bool more = n + 1 < n_iter;
-    if (more) {
-      issue(n + 1, stage ^ 1);
-      if (tid < KBM) nxt = load_info(n + 1);
-    }
-    const int st = n % nsteps;
-    const int qs = it.q_begin + st * KBM;
-    if (wave_live) {
-      const __bf16* sQ = sQD[stage][0];
-      const __bf16* sdO = sQD[stage][1];
-      const QInfo* inf = sInfo[stage];
+    wait_tile<NS, PER_STEP>(n, n_iter);
+    __syncthreads();  // step n landed; the stage of step n-1 is free
+    if (n + NS - 1 < n_iter) issue(n + NS - 1);
+    if (!wave_live) continue;
+    const DkdvStage<D>& sg = st[n % NS];
+    const int qs = it.q_begin + (n % nsteps) * KBM;
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        // queries past the range sit at the end of a block; a block whose first
-        // query is not real, or whose last real query precedes every key of the
-        // wave, has no visible pair
-        if (inf[qb * 32].hi < 0) continue;
-        const int blk_last = min(qs + qb * 32 + 31, min(it.q_end, it.valid) - 1);
-        if (blk_last < wk0) continue;
-        f32x16 s = f32x16{}, dp = f32x16{};
+    for (int qb = 0; qb < 2; ++qb) {
+      // a block with no real query, or whose last real query precedes every key
+      // of the wave, has no visible pair
+      const int qb0 = qs + qb * 32;
+      if (qb0 >= qlim) continue;
+      if (min(qb0 + 31, qlim - 1) < wk0) continue;
+      // operands of the first two products (16-byte row reads)
+      bf16x8 aq[D / 16], ad[D / 16];
 #pragma unroll
-        for (int c = 0; c < D / 16; ++c) s = mfma32(lds_row8<D>(sQ, qb * 32 + ln, 2 * c + hf), kf[c], s);
+      for (int c = 0; c < D / 16; ++c) {
+        aq[c] = lds_row8<D>(sg.q, qb * 32 + ln, 2 * c + hf);
+        ad[c] = lds_row8<D>(sg.dout, qb * 32 + ln, 2 * c + hf);
+      }
+      f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-        for (int c = 0; c < D / 16; ++c) dp = mfma32(lds_row8<D>(sdO, qb * 32 + ln, 2 * c + hf), vf[c], dp);
+      for (int c = 0; c < D / 16; ++c) {
+        s = mfma32(aq[c], kf[c], s);
+        dp = mfma32(ad[c], vf[c], dp);
+      }
+      // transposed operands of the last two products, requested before the
+      // softmax arithmetic so their latency hides behind it
+      bf16x8 tdo[D / 32][2], tq[D / 32][2];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const QInfo q = inf[qb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)];
-          const bool vis = (j <= q.hi) & ((j < it.P) | (j >= q.lo));
-          const float e = fast_exp2(fmaf(s[r], p.scale_log2, -q.lse2));
-          const float pr = vis ? e : 0.f;
-          s[r] = pr;
-          dp[r] = pr * (dp[r] - q.delta);
+      for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+          tdo[m][h2] = lds_tr8<D>(sg.dout, qb * 32 + 16 * h2, 32 * m, lane);
+          tq[m][h2] = lds_tr8<D>(sg.q, qb * 32 + 16 * h2, 32 * m, lane);
         }
-        const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
-        const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
 #pragma unroll
-        for (int m = 0; m < D / 32; ++m) {
-          acc_dv[m] = mfma32(lds_tr8<D>(sdO, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
-          acc_dv[m] = mfma32(lds_tr8<D>(sdO, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
-          acc_dk[m] = mfma32(lds_tr8<D>(sQ, qb * 32, 32 * m, lane), db0, acc_dk[m]);
-          acc_dk[m] = mfma32(lds_tr8<D>(sQ, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int il = qb * 32 + 8 * r4 + 4 * hf;  // rows il .. il+3 of this register group
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sg.lse[il]);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sg.delta[il]);
+        typedef int i32x4 __attribute__((ext_vector_type(4)));
+        const i32x4 o4 = *reinterpret_cast<const i32x4*>(&sg.seg_lo[il]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 4 * r4 + e;
+          const int qi = qs + il + e;
+          const unsigned hole = o4[e] > it.P ? (unsigned)(o4[e] - it.P) : 0u;
+          const bool vis = (j <= qi) & (qi < qlim) & (jP >= hole);
+          const float ex = fast_exp2(fmaf(s[r], p.scale_log2, -l4[e] * kLog2e));
+          const float pr = vis ? ex : 0.f;
+          s[r] = pr;
+          dp[r] = pr * (dp[r] - d4[e]);
         }
       }
+      const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
+      const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
+#pragma unroll
+      for (int m = 0; m < D / 32; ++m) {
+        acc_dv[m] = mfma32(tdo[m][0], pb0, acc_dv[m]);
+        acc_dk[m] = mfma32(tq[m][0], db0, acc_dk[m]);
+        acc_dv[m] = mfma32(tdo[m][1], pb1, acc_dv[m]);
+        acc_dk[m] = mfma32(tq[m][1], db1, acc_dk[m]);
+      }
     }
-    if (more && tid < KBM) sInfo[stage ^ 1][tid] = nxt;
   }
 
   if (!k_in_tile) return;
@@ -238,12 +256,13 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
 // dQ: query-major
 // ---------------------------------------------------------------------------
 
-constexpr int QBM = kDqBlockM;  // 128
 constexpr int QBN = kDqBlockN;  // 64
 
-template <int D, typename TO>
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
-  __shared__ __attribute__((aligned(1024))) __bf16 sKV[2][2][QBN * D];
+template <int D, int NW, int NS, typename TO>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p) {
+  constexpr int RPW = QBN / NW;
+  using Dma = TileDma<D, RPW>;
+  __shared__ __attribute__((aligned(1024))) __bf16 sKV[NS][2][QBN * D];
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
@@ -262,21 +281,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
   const bool real = i < it.valid;
   const int hi = real ? i : -1;
   const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
+  const unsigned hole = (real && lo > it.P) ? (unsigned)(lo - it.P) : 0u;
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
-
-  const int64_t kv_stride = (int64_t)p.hkv * D;
-  const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
-  const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
-  const int kv_lim = it.valid;
-  const int n_tiles = it.kt_cnt;
-
-  if (n_tiles > 0) {
-    const int k0 = p.dq_ktiles[it.kt_off];
-    const int rows = min(QBN, kv_lim - k0);
-    dma_rows<D, QBN / 4>(sKV[0][0], kbase + k0 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
-    dma_rows<D, QBN / 4>(sKV[0][1], vbase + k0 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
-  }
-
   const float lse2 = real ? p.lse[(int64_t)head * p.sumT + it.tok0 + i] * kLog2e : 0.f;
   const float dlt = real ? p.delta[(int64_t)head * p.sumT + it.tok0 + i] : 0.f;
   bf16x8 qf[D / 16], df[D / 16];
@@ -285,6 +291,24 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
     qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
     df[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.dout + qrow * D + 16 * c + 8 * hf) : bf16x8{};
   }
+
+  const int64_t kv_stride = (int64_t)p.hkv * D;
+  const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const int kv_lim = it.valid;
+  const int n_tiles = it.kt_cnt;
+  Dma dma;
+  dma.init(wave * RPW, kv_stride, lane);
+  auto issue = [&](int t) {
+    const int k0 = p.dq_ktiles[it.kt_off + t];
+    const int rows = min(QBN, kv_lim - k0);
+    dma.issue(sKV[t % NS][0], kbase + k0 * kv_stride, rows);
+    dma.issue(sKV[t % NS][1], vbase + k0 * kv_stride, rows);
+  };
+#pragma unroll
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < n_tiles) issue(t);
+
   f32x16 acc[D / 32];
 #pragma unroll
   for (int m = 0; m < D / 32; ++m) acc[m] = f32x16{};
@@ -293,17 +317,12 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
 
   for (int t = 0; t < n_tiles; ++t) {
     const int k0 = p.dq_ktiles[it.kt_off + t];
-    wait_vmem_all();
+    wait_tile<NS, 2 * Dma::N>(t, n_tiles);
     __syncthreads();
-    if (t + 1 < n_tiles) {
-      const int k1 = p.dq_ktiles[it.kt_off + t + 1];
-      const int rows = min(QBN, kv_lim - k1);
-      dma_rows<D, QBN / 4>(sKV[(t + 1) & 1][0], kbase + k1 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
-      dma_rows<D, QBN / 4>(sKV[(t + 1) & 1][1], vbase + k1 * kv_stride, kv_stride, wave * (QBN / 4), rows, lane);
-    }
+    if (t + NS - 1 < n_tiles) issue(t + NS - 1);
     if (!wave_live) continue;
-    const __bf16* sK = sKV[t & 1][0];
-    const __bf16* sV = sKV[t & 1][1];
+    const __bf16* sK = sKV[t % NS][0];
+    const __bf16* sV = sKV[t % NS][1];
 
     const int k_last = k0 + QBN - 1;
     const bool lane_any = in_tile && hi >= k0 && (k0 < it.P || max(k0, lo) <= min(hi, k_last));
@@ -321,12 +340,13 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(BwdParams<TO> p) {
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) dp[kb] = mfma32(lds_row8<D>(sV, kb * 32 + ln, 2 * c + hf), df[c], dp[kb]);
     }
+    const int jb = k0 + 4 * hf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int jj = k0 + kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-        const bool vis = (!need_mask) | ((jj <= hi) & ((jj < it.P) | (jj >= lo)));
+        const int jj = jb + kb * 32 + 8 * (r >> 2) + (r & 3);
+        const bool vis = (!need_mask) | ((jj <= hi) & ((unsigned)(jj - it.P) >= hole));
         const float e = fast_exp2(fmaf(s[kb][r], p.scale_log2, -lse2));
         const float pr = vis ? e : 0.f;
         dp[kb][r] = pr * (dp[kb][r] - dlt);
@@ -390,14 +410,14 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dkdv", s);
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(256),
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, kDkdvStages, TO>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(256),
                        0, s, p);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dq", s);
-    hipLaunchKernelGGL((bwd_dq_kernel<D, TO>), dim3((unsigned)((int64_t)a.n_dq_items * a.hq)), dim3(256), 0,
+    hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqStages, TO>), dim3((unsigned)((int64_t)a.n_dq_items * a.hq)), dim3(kDqWaves * 64), 0,
                        s, p);
   }
   return hipGetLastError();

@@ -1,17 +1,17 @@
 // Forward attention over preference-packed rows (Sec. 3.2) on gfx950.
 //
-// One workgroup = one query tile of 128 queries of one row and one query head;
-// its four waves own 32 queries each.  The workgroup walks the tile's list of
-// 64-key tiles that hold a visible pair (tiles whose every pair is masked --
-// the causal upper triangle and a response's view of its siblings -- are never
-// listed).  Per key tile:
+// One workgroup = one query tile of 32*NW queries of one row and one query
+// head; each of its NW waves owns 32 queries.  The workgroup walks the tile's
+// list of 64-key tiles that hold a visible pair (tiles whose every pair is
+// masked -- the causal upper triangle and a response's view of its siblings --
+// are never listed).  Per key tile:
 //
-//   * K and V are DMA'd (global_load_lds) into a double-buffered, swizzled LDS
-//     stage while the previous tile is being computed: one barrier per tile;
+//   * K and V are DMA'd (global_load_lds) into an NS-deep ring of swizzled LDS
+//     stages, NS-1 tiles ahead of the one being computed: one barrier per tile;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: lane l owns query l%32, so the
 //     softmax row statistics stay in the lane (one cross-half exchange);
 //   * the mask is evaluated only when the tile is not fully visible to the
-//     wave: visible(i, j) = j <= hi_i && (j < P || j >= lo_i);
+//     wave: visible(i, j) = j <= hi_i && j is not in [P, lo_i);
 //   * base-2 online softmax with scale*log2(e) folded in; the running maximum
 //     is only raised when a tile exceeds it by more than 2^8, so most tiles
 //     skip the rescale of O;
@@ -29,7 +29,6 @@
 namespace pp {
 namespace {
 
-constexpr int BM = kFwdBlockM;  // 128
 constexpr int BN = kFwdBlockN;  // 64
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 
@@ -48,9 +47,11 @@ struct FwdParams {
   float scale_log2;
 };
 
-template <int D, typename TO>
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
-  __shared__ __attribute__((aligned(1024))) __bf16 sKV[2][2][BN * D];  // [stage][K/V][row*D]
+template <int D, int NW, int NS, typename TO>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO> p) {
+  constexpr int RPW = BN / NW;  // tile rows each wave fetches
+  using Dma = TileDma<D, RPW>;
+  __shared__ __attribute__((aligned(1024))) __bf16 sKV[NS][2][BN * D];  // [stage][K/V][row*D]
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
@@ -69,26 +70,32 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
   const bool real = i < it.valid;
   const int hi = real ? i : -1;
   const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
+  // key j lies in the "hole" [P, lo) that a response query cannot see iff
+  // (unsigned)(j - P) < (unsigned)(lo - P); a prompt query (lo = 0) has no hole.
+  const unsigned hole = (real && lo > it.P) ? (unsigned)(lo - it.P) : 0u;
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
+
+  bf16x8 qf[D / 16];
+#pragma unroll
+  for (int c = 0; c < D / 16; ++c)
+    qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
 
   const int64_t kv_stride = (int64_t)p.hkv * D;
   const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
   const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
   const int kv_lim = it.valid;
   const int n_tiles = it.kt_cnt;
-
-  // prologue: first key tile in flight before Q is read
-  if (n_tiles > 0) {
-    const int k0 = p.ktiles[it.kt_off];
+  Dma dma;
+  dma.init(wave * RPW, kv_stride, lane);
+  auto issue = [&](int t) {
+    const int k0 = p.ktiles[it.kt_off + t];
     const int rows = min(BN, kv_lim - k0);
-    dma_rows<D, BN / 4>(sKV[0][0], kbase + k0 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
-    dma_rows<D, BN / 4>(sKV[0][1], vbase + k0 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
-  }
-
-  bf16x8 qf[D / 16];
+    dma.issue(sKV[t % NS][0], kbase + k0 * kv_stride, rows);
+    dma.issue(sKV[t % NS][1], vbase + k0 * kv_stride, rows);
+  };
 #pragma unroll
-  for (int c = 0; c < D / 16; ++c)
-    qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
+  for (int t = 0; t < NS - 1; ++t)
+    if (t < n_tiles) issue(t);
 
   f32x16 acc_o[D / 32];
 #pragma unroll
@@ -101,17 +108,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
 
   for (int t = 0; t < n_tiles; ++t) {
     const int k0 = p.ktiles[it.kt_off + t];
-    wait_vmem_all();
-    __syncthreads();  // tile t landed for every wave; stage (t+1)&1 is free
-    if (t + 1 < n_tiles) {
-      const int k1 = p.ktiles[it.kt_off + t + 1];
-      const int rows = min(BN, kv_lim - k1);
-      dma_rows<D, BN / 4>(sKV[(t + 1) & 1][0], kbase + k1 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
-      dma_rows<D, BN / 4>(sKV[(t + 1) & 1][1], vbase + k1 * kv_stride, kv_stride, wave * (BN / 4), rows, lane);
-    }
+    wait_tile<NS, 2 * Dma::N>(t, n_tiles);
+    __syncthreads();  // tile t landed for every wave; the stage of tile t-1 is free
+    if (t + NS - 1 < n_tiles) issue(t + NS - 1);
     if (!wave_live) continue;
-    const __bf16* sK = sKV[t & 1][0];
-    const __bf16* sV = sKV[t & 1][1];
+    const __bf16* sK = sKV[t % NS][0];
+    const __bf16* sV = sKV[t % NS][1];
 
     const int k_last = k0 + BN - 1;
     const bool lane_any = in_tile && hi >= k0 && (k0 < it.P || max(k0, lo) <= min(hi, k_last));
@@ -128,12 +130,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams<TO> p) {
       for (int c = 0; c < D / 16; ++c) s[kb] = mfma32(lds_row8<D>(sK, kb * 32 + ln, 2 * c + hf), qf[c], s[kb]);
     }
     if (need_mask) {
+      const int jb = k0 + 4 * hf;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int j = k0 + kb * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-          const bool vis = (j <= hi) & ((j < it.P) | (j >= lo));
+          const int j = jb + kb * 32 + 8 * (r >> 2) + (r & 3);
+          const bool vis = (j <= hi) & ((unsigned)(j - it.P) >= hole);
           s[kb][r] = vis ? s[kb][r] : kNegInf;
         }
     }
@@ -229,7 +232,8 @@ hipError_t launch_fwd_t(const AttnFwdLaunch& a, hipStream_t s) {
   const int64_t blocks = (int64_t)a.n_items * a.hq;
   if (blocks == 0) return hipSuccess;
   TimingScope t("pp_attn_fwd", s);
-  hipLaunchKernelGGL((attn_fwd_kernel<D, TO>), dim3((unsigned)blocks), dim3(256), 0, s, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdWaves, kFwdStages, TO>), dim3((unsigned)blocks),
+                     dim3(kFwdWaves * 64), 0, s, p);
   return hipGetLastError();
 }
 

@@ -77,19 +77,10 @@ __device__ __forceinline__ bf16x8 to_bf16x8(float a0, float a1, float a2, float 
 // 16s + 8*(e/4) + 4h + e%4 for e = 0..7, i.e. the contraction index
 // kk = 8h + e stands for row 16s + perm16(kk) with
 //   perm16(kk) = 8*((kk%8)/4) + 4*(kk/8) + kk%4.
-// An A operand read from LDS must use the same order, which the kernels get by
-// storing groups of four rows at position kRowGroupPos[group] inside each
-// 16-row chunk: rows 0-3 -> 0, 4-7 -> 8, 8-11 -> 4, 12-15 -> 12.
+// An A operand read from LDS must use the same row order (see lds_tr8).
 __device__ __forceinline__ bf16x8 acc_half_to_bf16(const f32x16& acc, int s) {
   return to_bf16x8(acc[8 * s + 0], acc[8 * s + 1], acc[8 * s + 2], acc[8 * s + 3], acc[8 * s + 4],
                    acc[8 * s + 5], acc[8 * s + 6], acc[8 * s + 7]);
-}
-
-__device__ __forceinline__ int row_group_pos(int group) {
-  // position of the 4-row group `group` inside its 16-row chunk, plus the chunk base
-  const int g = group & 3;
-  const int p = (g == 0) ? 0 : (g == 1) ? 8 : (g == 2) ? 4 : 12;
-  return (group >> 2) * 16 + p;
 }
 
 // ---------------------------------------------------------------------------
@@ -112,26 +103,63 @@ __device__ __forceinline__ int swz(int r) {
   else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
 }
 
-// Wave-cooperative DMA of rows [row0, row0 + NR) of a tile into LDS.  Row r of
-// the tile comes from `src + min(r, rows_valid - 1) * stride` (elements), so rows
-// past the valid range repeat the last valid row (finite data that the mask
-// then ignores).  NR * D * 2 must be a multiple of 1 KB.
+// Wave-cooperative DMA of NR tile rows [row0, row0 + NR) into LDS.  Tile row r
+// comes from `src + min(r, rows_valid - 1) * stride` (elements), so rows past
+// the valid range repeat the last valid row (finite data that the mask then
+// ignores).  NR * D * 2 must be a multiple of 1 KB.  The per-lane part of the
+// addresses is computed once (`init`); `issue` then only adds the tile base.
 template <int D, int NR>
-__device__ __forceinline__ void dma_rows(__bf16* lds_tile, const __bf16* src, int64_t stride, int row0,
-                                         int rows_valid, int lane) {
-  constexpr int RPI = 1024 / (D * 2);  // rows per wave instruction
-  constexpr int CPR = D / 8;           // 16-byte chunks per row
+struct TileDma {
+  static constexpr int RPI = 1024 / (D * 2);  // rows per wave instruction
+  static constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static constexpr int N = NR / RPI;          // instructions per call
   static_assert(NR % RPI == 0, "tile rows must fill whole wave loads");
+  int off[N];   // element offset of this lane's chunk in instruction i, full tile
+  int64_t stride;
+  int row0;
+  int lane;
+
+  // tile row and 8 * logical chunk that this lane fetches in instruction i
+  __device__ __forceinline__ int row_of(int i) const { return row0 + i * RPI + lane / CPR; }
+  __device__ __forceinline__ int chunk8_of(int i) const { return ((lane % CPR) ^ swz<D>(row_of(i))) << 3; }
+
+  __device__ __forceinline__ void init(int row0_, int64_t stride_, int lane_) {
+    row0 = row0_;
+    stride = stride_;
+    lane = lane_;
 #pragma unroll
-  for (int i = 0; i < NR / RPI; ++i) {
-    const int rb = row0 + i * RPI;
-    const int r = rb + lane / CPR;
-    const int pc = lane % CPR;
-    const int lc = pc ^ swz<D>(r);
-    const int rs = min(r, rows_valid - 1);
-    __builtin_amdgcn_global_load_lds((const void*)(src + rs * stride + lc * 8),
-                                     (lds_void*)(lds_tile + rb * D), 16, 0, 0);
+    for (int i = 0; i < N; ++i) off[i] = (int)(row_of(i) * stride) + chunk8_of(i);
   }
+
+  __device__ __forceinline__ void issue(__bf16* lds_tile, const __bf16* src, int rows_valid) const {
+    if (rows_valid >= row0 + N * RPI) {
+#pragma unroll
+      for (int i = 0; i < N; ++i)
+        __builtin_amdgcn_global_load_lds((const void*)(src + off[i]),
+                                         (lds_void*)(lds_tile + (row0 + i * RPI) * D), 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int rs = min(row_of(i), rows_valid - 1);
+        __builtin_amdgcn_global_load_lds((const void*)(src + rs * stride + chunk8_of(i)),
+                                         (lds_void*)(lds_tile + (row0 + i * RPI) * D), 16, 0, 0);
+      }
+    }
+  }
+};
+
+// One 4-byte element per lane into LDS (lane l -> lds + 4*l): the per-query
+// scalars of a 64-query tile.
+__device__ __forceinline__ void dma_dword(void* lds, const void* src) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds, 4, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // 16-byte read of logical chunk `lc` (elements 8*lc .. 8*lc+7) of tile row r.
@@ -166,7 +194,23 @@ __device__ __forceinline__ bf16x8 lds_tr8(const __bf16* tile, int row16, int col
   return __builtin_bit_cast(bf16x8, v);
 }
 
-__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0); }
+// Waits until pipelined tile t has landed, given that tiles t+1 ..
+// min(t+NS-2, n-1) (each PER_TILE DMA instructions of this wave, issued after
+// tile t) may still be in flight.  Vector-memory loads complete in order.
+template <int NS, int PER_TILE>
+__device__ __forceinline__ void wait_tile(int t, int n) {
+  if constexpr (NS == 2) {
+    wait_vmem<0>();
+  } else if constexpr (NS == 3) {
+    if (t + 1 < n) wait_vmem<PER_TILE>();
+    else wait_vmem<0>();
+  } else {
+    static_assert(NS == 4, "pipeline depth 2, 3 or 4");
+    if (t + 2 < n) wait_vmem<2 * PER_TILE>();
+    else if (t + 1 < n) wait_vmem<PER_TILE>();
+    else wait_vmem<0>();
+  }
+}
 
 __device__ __forceinline__ float wave_max(float x) {
   for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));

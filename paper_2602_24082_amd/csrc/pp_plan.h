@@ -19,13 +19,38 @@
 
 namespace pp {
 
-// Tile sizes of the kernels (rows of the flat token axis).
-constexpr int kFwdBlockM = 128;   // queries per forward workgroup (4 waves x 32)
-constexpr int kFwdBlockN = 64;    // keys per forward k-tile
-constexpr int kDqBlockM = 128;    // queries per dQ workgroup
-constexpr int kDqBlockN = 64;     // keys per dQ k-tile
-constexpr int kBwdBlockN = 128;   // keys per dK/dV workgroup (4 waves x 32)
-constexpr int kBwdBlockM = 64;    // queries per dK/dV inner step
+// Launch shapes: waves per workgroup and LDS pipeline depth (key or query
+// tiles in flight) of each attention kernel.
+#ifndef PP_FWD_WAVES
+#define PP_FWD_WAVES 4
+#endif
+#ifndef PP_FWD_STAGES
+#define PP_FWD_STAGES 2
+#endif
+#ifndef PP_DQ_WAVES
+#define PP_DQ_WAVES 4
+#endif
+#ifndef PP_DQ_STAGES
+#define PP_DQ_STAGES 2
+#endif
+#ifndef PP_DKDV_STAGES
+#define PP_DKDV_STAGES 2
+#endif
+
+// Tile sizes of the kernels (rows of the flat token axis).  Each wave of the
+// forward and dQ kernels owns 32 queries; each wave of the dK/dV kernel owns
+// 32 keys.
+constexpr int kFwdWaves = PP_FWD_WAVES;
+constexpr int kFwdStages = PP_FWD_STAGES;
+constexpr int kDqWaves = PP_DQ_WAVES;
+constexpr int kDqStages = PP_DQ_STAGES;
+constexpr int kDkdvStages = PP_DKDV_STAGES;
+constexpr int kFwdBlockM = 32 * kFwdWaves;  // queries per forward workgroup
+constexpr int kFwdBlockN = 64;              // keys per forward k-tile
+constexpr int kDqBlockM = 32 * kDqWaves;    // queries per dQ workgroup
+constexpr int kDqBlockN = 64;               // keys per dQ k-tile
+constexpr int kBwdBlockN = 128;             // keys per dK/dV workgroup (4 waves x 32)
+constexpr int kBwdBlockM = 64;              // queries per dK/dV inner step
 
 // One query tile: queries [q0, q_end) of the row starting at flat index tok0.
 struct QTileItem {
