@@ -256,7 +256,8 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
 // dQ: query-major
 // ---------------------------------------------------------------------------
 
-constexpr int QBN = kDqBlockN;  // 64
+constexpr int QBN = kDqBlockN;  // 32 or 64
+constexpr int QKB = QBN / 32;   // 32-key blocks per tile
 
 template <int D, int NW, int NS, typename TO>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p) {
@@ -330,9 +331,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
     if (!__any(lane_any)) continue;
     const bool need_mask = !__all(lane_all);
 
-    f32x16 s[2], dp[2];
+    f32x16 s[QKB], dp[QKB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < QKB; ++kb) {
       s[kb] = f32x16{};
       dp[kb] = f32x16{};
 #pragma unroll
@@ -342,7 +343,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
     }
     const int jb = k0 + 4 * hf;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < QKB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = jb + kb * 32 + 8 * (r >> 2) + (r & 3);
@@ -351,14 +352,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
         const float pr = vis ? e : 0.f;
         dp[kb][r] = pr * (dp[kb][r] - dlt);
       }
-    bf16x8 db[4];
+    bf16x8 db[2 * QKB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < QKB; ++kb) {
       db[2 * kb] = acc_half_to_bf16(dp[kb], 0);
       db[2 * kb + 1] = acc_half_to_bf16(dp[kb], 1);
     }
 #pragma unroll
-    for (int ch = 0; ch < 4; ++ch)
+    for (int ch = 0; ch < 2 * QKB; ++ch)
 #pragma unroll
       for (int m = 0; m < D / 32; ++m) acc[m] = mfma32(lds_tr8<D>(sK, 16 * ch, 32 * m, lane), db[ch], acc[m]);
   }

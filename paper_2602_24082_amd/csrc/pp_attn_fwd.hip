@@ -2,7 +2,7 @@
 //
 // One workgroup = one query tile of 32*NW queries of one row and one query
 // head; each of its NW waves owns 32 queries.  The workgroup walks the tile's
-// list of 64-key tiles that hold a visible pair (tiles whose every pair is
+// list of BN-key tiles (BN = 32 or 64) that hold a visible pair (tiles whose every pair is
 // masked -- the causal upper triangle and a response's view of its siblings --
 // are never listed).  Per key tile:
 //
@@ -29,7 +29,8 @@
 namespace pp {
 namespace {
 
-constexpr int BN = kFwdBlockN;  // 64
+constexpr int BN = kFwdBlockN;  // 32 or 64
+constexpr int KB = BN / 32;     // 32-key blocks per tile
 constexpr float kRescaleSlack = 8.0f;  // log2 units
 
 template <typename TO>
@@ -121,10 +122,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
     if (!__any(lane_any)) continue;
     const bool need_mask = !__all(lane_all);
 
-    // ---- S^T = K Q^T : two 32-key blocks
-    f32x16 s[2];
+    // ---- S^T = K Q^T, one 32x32 block per 32 keys
+    f32x16 s[KB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
       s[kb] = f32x16{};
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) s[kb] = mfma32(lds_row8<D>(sK, kb * 32 + ln, 2 * c + hf), qf[c], s[kb]);
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
     if (need_mask) {
       const int jb = k0 + 4 * hf;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int j = jb + kb * 32 + 8 * (r >> 2) + (r & 3);
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
     // ---- online softmax with a lazily raised reference maximum
     float mx = kNegInf;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
     const float mref = (m_ref == kNegInf) ? 0.f : m_ref;
     float psum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float e = fast_exp2(fmaf(s[kb][r], c2, -mref));
@@ -172,15 +173,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
       }
     l_run += psum;
 
-    // ---- O^T += V^T P^T over four 16-key chunks
-    bf16x8 pb[4];
+    // ---- O^T += V^T P^T over 16-key chunks
+    bf16x8 pb[2 * KB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KB; ++kb) {
       pb[2 * kb] = acc_half_to_bf16(s[kb], 0);
       pb[2 * kb + 1] = acc_half_to_bf16(s[kb], 1);
     }
 #pragma unroll
-    for (int ch = 0; ch < 4; ++ch)
+    for (int ch = 0; ch < 2 * KB; ++ch)
 #pragma unroll
       for (int m = 0; m < D / 32; ++m) acc_o[m] = mfma32(lds_tr8<D>(sV, 16 * ch, 32 * m, lane), pb[ch], acc_o[m]);
   }

@@ -36,6 +36,12 @@ namespace pp {
 #ifndef PP_DKDV_STAGES
 #define PP_DKDV_STAGES 2
 #endif
+#ifndef PP_FWD_BLOCK_N
+#define PP_FWD_BLOCK_N 64
+#endif
+#ifndef PP_DQ_BLOCK_N
+#define PP_DQ_BLOCK_N 64
+#endif
 
 // Tile sizes of the kernels (rows of the flat token axis).  Each wave of the
 // forward and dQ kernels owns 32 queries; each wave of the dK/dV kernel owns
@@ -46,9 +52,9 @@ constexpr int kDqWaves = PP_DQ_WAVES;
 constexpr int kDqStages = PP_DQ_STAGES;
 constexpr int kDkdvStages = PP_DKDV_STAGES;
 constexpr int kFwdBlockM = 32 * kFwdWaves;  // queries per forward workgroup
-constexpr int kFwdBlockN = 64;              // keys per forward k-tile
+constexpr int kFwdBlockN = PP_FWD_BLOCK_N;  // keys per forward k-tile (32 or 64)
 constexpr int kDqBlockM = 32 * kDqWaves;    // queries per dQ workgroup
-constexpr int kDqBlockN = 64;               // keys per dQ k-tile
+constexpr int kDqBlockN = PP_DQ_BLOCK_N;    // keys per dQ k-tile (32 or 64)
 constexpr int kBwdBlockN = 128;             // keys per dK/dV workgroup (4 waves x 32)
 constexpr int kBwdBlockM = 64;              // queries per dK/dV inner step
 

@@ -1,0 +1,140 @@
+"""Full-size GPU parity on sampled outputs.
+
+The kernels run on whole batches of the benchmarked workloads, in the launch
+configuration the benchmark times; the fp64 oracle then recomputes a sample
+it can afford -- one row (rows are independent) and one kv-head group (heads
+are independent), or single responses for the log-probabilities -- and the
+two are compared element by element with the same tolerances as the small
+parity tests.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import pp_oracle as orc
+from paper_2602_24082_amd import binding as pp
+from paper_2602_24082_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _row_pack(pack, b):
+    K = int(pack.num_resp[b])
+    return wl.make_pack([int(pack.prompt_len[b])], [pack.resp_len[b, :K].tolist()],
+                        pad=[int(pack.row_lengths()[b]) - int(pack.prompt_len[b]) - int(pack.resp_len[b, :K].sum())])
+
+
+def _attention_sample(cfg_index, group):
+    cfg = wl.CONFIGS[cfg_index]
+    pack = wl.config_pack(cfg)
+    seed = wl.tensor_seed(cfg.index, 0)
+    q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, seed, torch.bfloat16, DEV)
+    o, lse = pp.pp_attn_fwd(pack, q, k, v)
+    dq, dk, dv = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+    torch.cuda.synchronize()
+    b = int(np.argmin(pack.row_lengths()))        # the shortest row keeps the oracle cheap
+    r0, r1 = int(pack.row_start[b]), int(pack.row_start[b + 1])
+    G = cfg.hq // cfg.hkv
+    hs = slice(group * G, (group + 1) * G)
+    gs = slice(group, group + 1)
+    print(f"{cfg.name}: row {b} T={r1 - r0}, q-heads {hs.start}..{hs.stop - 1}, kv-head {group}", flush=True)
+    sub = lambda x, s: x[r0:r1, s].double().cpu().numpy()
+    row = _row_pack(pack, b)
+    args = row.oracle_args()
+    O_ref, L_ref = orc.attn_fwd(*args, sub(q, hs), sub(k, gs), sub(v, gs))
+    dq_r, dk_r, dv_r = orc.attn_bwd(*args, sub(q, hs), sub(k, gs), sub(v, gs), sub(do, hs))
+    o_c = sub(o, hs)
+    l_c = lse[hs, r0:r1].double().cpu().numpy()
+    assert np.abs(o_c - O_ref).max() <= 1e-2
+    assert np.abs(l_c - L_ref).max() <= 1e-2
+    for name, got, ref in (("dq", sub(dq, hs), dq_r), ("dk", sub(dk, gs), dk_r), ("dv", sub(dv, gs), dv_r)):
+        err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+        assert err <= 2e-2, (name, err)
+    # nothing left unwritten anywhere in the batch
+    for t in (o, lse, dq, dk, dv):
+        assert torch.isfinite(t).all()
+
+
+def test_fullsize_llama3_8b_attention():
+    _attention_sample(1, group=3)
+
+
+def test_fullsize_rm_k4_attention():
+    _attention_sample(2, group=5)
+
+
+def test_fullsize_long_prefix_attention():
+    _attention_sample(3, group=7)
+
+
+def test_fullsize_dpo_chain_attention():
+    _attention_sample(4, group=0)
+
+
+def _compact_response(pack, b, k, logits, tokens):
+    """One response as its own pack: the predicting row P-1 then the rows that
+    predict tokens 2..L, with the response's labels (the oracle's index rule
+    maps the compact pack onto exactly these rows)."""
+    r0 = int(pack.row_start[b])
+    P = int(pack.prompt_len[b])
+    o, L = int(pack.resp_off[b, k]), int(pack.resp_len[b, k])
+    rows = [r0 + P - 1] + [r0 + o + j - 1 for j in range(1, L)]
+    lg = logits[rows].double().cpu().numpy()
+    lab = np.zeros(1 + L, np.int64)
+    lab[1:] = tokens[r0 + o:r0 + o + L].cpu().numpy()
+    # compact layout: prompt of 1 token (row 0 = the last prompt position), then the
+    # response; row 1 + j - 1 predicts token 1 + j
+    lg_full = np.zeros((1 + L, lg.shape[1]))
+    lg_full[0] = lg[0]
+    lg_full[1:L] = lg[1:]
+    cp = wl.make_pack([1], [[L]])
+    seq, _ = orc.seq_logprob(*cp.oracle_args(), lg_full, lab)
+    return seq[0, 0]
+
+
+def _logprob_sample(cfg_index, stream, n_samples=6):
+    cfg = wl.CONFIGS[cfg_index]
+    pack = wl.config_pack(cfg)
+    seed = wl.tensor_seed(cfg.index, 0)
+    T = pack.total_tokens
+    logits = wl.randn_rows(T, cfg.vocab, seed + stream, torch.bfloat16, DEV, cfg.logit_sigma)
+    tokens = wl.randint((T,), cfg.vocab, seed + wl.STREAM_TOKENS, DEV)
+    seq, tok = pp.pp_seq_logprob(pack, logits, tokens, want_tok=True)
+    torch.cuda.synchronize()
+    seq_c = seq.double().cpu().numpy()
+    tok_c = tok.double().cpu().numpy()
+    rng = np.random.default_rng(cfg_index)
+    picks = [(int(b), int(rng.integers(0, int(pack.num_resp[b])))) for b in rng.integers(0, pack.num_rows, n_samples)]
+    for b, k in picks:
+        want = _compact_response(pack, b, k, logits, tokens)
+        assert abs(seq_c[b, k] - want) <= 1e-4 * abs(want), (b, k, seq_c[b, k], want)
+    # every response's sum equals the sum of its per-token values (fp64 on host)
+    for b in range(pack.num_rows):
+        r0 = int(pack.row_start[b])
+        for k in range(int(pack.num_resp[b])):
+            o, L = int(pack.resp_off[b, k]), int(pack.resp_len[b, k])
+            s = tok_c[r0 + o:r0 + o + L].sum()
+            assert abs(seq_c[b, k] - s) <= 1e-5 * max(1.0, abs(s))
+    return pack, seq
+
+
+def test_fullsize_rm_k4_logprob_and_bt_loss():
+    pack, seq = _logprob_sample(2, wl.STREAM_LOGITS_POL)
+    cfg = wl.CONFIGS[2]
+    loss, rows, grad = pp.pp_dpo_loss(pack.num_resp.tolist(), seq, None, cfg.beta)
+    want, want_rows, want_g = orc.pair_loss(pack.num_resp.tolist(), seq.double().cpu().numpy(), None, cfg.beta)
+    assert abs(float(loss) - want) <= 1e-4 * abs(want)
+    assert np.allclose(grad.cpu().numpy(), want_g, rtol=1e-4, atol=1e-7)
+
+
+def test_fullsize_dpo_chain_logprob_and_loss():
+    pack, s_pol = _logprob_sample(4, wl.STREAM_LOGITS_POL, n_samples=4)
+    _, s_ref = _logprob_sample(4, wl.STREAM_LOGITS_REF, n_samples=4)
+    cfg = wl.CONFIGS[4]
+    loss, rows, grad = pp.pp_dpo_loss(pack.num_resp.tolist(), s_pol, s_ref, cfg.beta)
+    want, want_rows, want_g = orc.pair_loss(pack.num_resp.tolist(), s_pol.double().cpu().numpy(),
+                                            s_ref.double().cpu().numpy(), cfg.beta)
+    assert abs(float(loss) - want) <= 1e-4 * abs(want)
+    assert np.allclose(rows.cpu().numpy(), want_rows, rtol=1e-4, atol=1e-7)
