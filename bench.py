@@ -25,6 +25,7 @@ kernels on the unpacked, prompt-duplicated, padded layout.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -45,6 +46,38 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (vendor)
 LOGPROB_VOCAB = 128256      # Llama-3 vocabulary for the 8B-shaped workload
 LOGPROB_SIGMA = 3.0
 DPO_BETA = 0.1
+
+
+CSRC = os.path.join(ROOT, "paper_2602_24082_amd", "csrc")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_dpo_step_llama3_8b_gqa32x8_d128.txt")
+
+
+def source_hash() -> str:
+    """sha256 over the HIP/C++ sources of the library (names and contents)."""
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(CSRC)):
+        h.update(fn.encode())
+        with open(os.path.join(CSRC, fn), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_from_profile(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when there is none or the sources changed since it was taken."""
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    rec, digest = {}, None
+    for line in open(TRAFFIC_PROFILE):
+        if line.startswith("source_sha256:"):
+            digest = line.split(":", 1)[1].strip()
+        elif line.startswith("kernel "):
+            parts = line.split()
+            kv = dict(x.split("=") for x in parts[2:])
+            rec[parts[1]] = int(float(kv["hbm_bytes"]))
+    if digest != source_hash():
+        return None
+    return rec.get(kernel)
 
 
 def useful_pairs(pack: wl.Pack) -> int:
@@ -132,6 +165,93 @@ def cpu_baseline(pack, cfg, rows, seed):
                        f"host has {len(os.sched_getaffinity(0))} usable cores")}
 
 
+def chain_sorting(dev, reps=1):
+    """The full DPO kernel chain (attention fwd+bwd, policy and reference
+    log-probs, loss) of the 72B-shaped workload: a pool of 128 samples cut into 8
+    batches of 16 rows, in draw order ("unsorted") or by packed length
+    ("sorted"), on the packed layout and on the unpacked layout (every
+    (prompt, response) pair its own sequence: attention padded to the batch's
+    longest pair, log-probs over the unpadded pairs).  Reports the single-GPU
+    total over the 8 batches and a simulated 8-rank data-parallel step (each
+    virtual rank runs 2 rows; a step costs its slowest rank)."""
+    cfg = wl.CONFIGS[4]
+    P, L, unsorted, sorted_b = wl.dpo_chain_pool(cfg)
+    V = cfg.vocab
+    max_tokens = 0
+    layouts = {}
+    for name, batches in (("unsorted", unsorted), ("sorted", sorted_b)):
+        for bi, rows in enumerate(batches):
+            pk = wl.make_pack([P[i] for i in rows], [L[i] for i in rows])
+            lp_pack = wl.make_pack([P[i] for i in rows for _ in L[i]], [[l] for i in rows for l in L[i]])
+            layouts[(name, bi)] = (pk, wl.unpacked_padded(pk), lp_pack, rows)
+            max_tokens = max(max_tokens, pk.total_tokens, lp_pack.total_tokens)
+    logits = [wl.randn_rows(max_tokens, V, 7 + m, torch.bfloat16, dev, cfg.logit_sigma) for m in range(2)]
+    tokens = wl.randint((max_tokens,), V, 9, dev)
+
+    def chain_ms(att_pack, lp_pack):
+        a = Attn(att_pack, cfg.hq, cfg.hkv, cfg.head_dim, 977, dev)
+        T = lp_pack.total_tokens
+        seqs = [torch.empty(lp_pack.num_rows, lp_pack.max_resp, dtype=torch.float32, device=dev) for _ in range(2)]
+        ws = torch.empty(pp.pp_workspace_size(lp_pack, vocab=V, fwd=False, bwd=False, logprob=True, loss=False)[2],
+                         dtype=torch.uint8, device=dev)
+        if lp_pack.max_resp >= 2:
+            num, pol, ref = lp_pack.num_resp.tolist(), seqs[0], seqs[1]
+        else:  # one response per row: regroup the K responses of each sample for the loss
+            num = None
+
+        def run():
+            a.run()
+            for m in range(2):
+                pp.pp_seq_logprob(lp_pack, logits[m][:T], tokens[:T], seq=seqs[m], ws=ws)
+            if num is not None:
+                pp.pp_dpo_loss(num, pol, ref, cfg.beta)
+            else:
+                k = 2
+                pp.pp_dpo_loss([k] * (lp_pack.num_rows // k), seqs[0].view(-1, k), seqs[1].view(-1, k), cfg.beta)
+        run()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(reps):
+            run()
+        e.record()
+        torch.cuda.synchronize()
+        del a
+        return s.elapsed_time(e) / reps
+
+    cells = {}
+    for name in ("unsorted", "sorted"):
+        for lay in ("packed", "unpacked_padded"):
+            total = 0.0
+            dp = 0.0
+            for bi in range(8):
+                pk, padded, lp_pack, rows = layouts[(name, bi)]
+                if lay == "packed":
+                    total += chain_ms(pk, pk)
+                else:
+                    total += chain_ms(padded, lp_pack)
+                ranks = []
+                for r in range(8):
+                    sub = rows[2 * r:2 * r + 2]
+                    spk = wl.make_pack([P[i] for i in sub], [L[i] for i in sub])
+                    if lay == "packed":
+                        ranks.append(chain_ms(spk, spk))
+                    else:
+                        slp = wl.make_pack([P[i] for i in sub for _ in L[i]], [[l] for i in sub for l in L[i]])
+                        ranks.append(chain_ms(wl.unpacked_padded(spk), slp))
+                dp += max(ranks)
+            cells[f"{lay}_{name}"] = {"one_gpu_ms": round(total, 3), "simulated_dp8_ms": round(dp, 3),
+                                      "one_gpu_samples_per_s": round(128 / (total * 1e-3), 1),
+                                      "simulated_dp8_samples_per_s": round(128 / (dp * 1e-3), 1)}
+    base = cells["unpacked_padded_unsorted"]
+    for c in cells.values():
+        c["one_gpu_speedup"] = round(base["one_gpu_ms"] / c["one_gpu_ms"], 3)
+        c["simulated_dp8_speedup"] = round(base["simulated_dp8_ms"] / c["simulated_dp8_ms"], 3)
+    print(json.dumps({"metric": "DPO kernel chain with batch sorting (72B-shaped, 128 samples, 8 batches of 16)",
+                      "unit": "ms", "data": "synthetic", "dtype": "bf16",
+                      "config": {"workload": cfg.name, "vocab": V, "beta": cfg.beta}, "cells": cells}))
+
+
 def calib_copy(dev):
     """A plain device copy of 1 GiB, five times: read 1 GiB + write 1 GiB each."""
     n = 1 << 30
@@ -153,6 +273,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
+    ap.add_argument("--chain-sorting", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the packed rows shard by "
@@ -164,6 +285,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.calib_copy:
         calib_copy(dev)
+        return
+    if args.chain_sorting:
+        chain_sorting(dev)
         return
 
     cfg = wl.CONFIGS[args.config]
@@ -237,16 +361,17 @@ def main():
     dom = max((k for k in kern if k in per_launch), key=lambda k: kern[k][0])
     bound, work = per_launch[dom]
     avg_ms = kern[dom][0] / kern[dom][1]
+    traffic = traffic_from_profile(dom) if args.config == 1 else None
     if bound == "mfma":
         ach = work / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                "avg_launch_ms": round(avg_ms, 4)}
+                "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                "algorithmic_flops_per_launch": work, "avg_launch_ms": round(avg_ms, 4)}
     else:
         ach = work / (avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
-                "avg_launch_ms": round(avg_ms, 4)}
+                "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic,
+                "algorithmic_bytes_per_launch": work, "avg_launch_ms": round(avg_ms, 4)}
     kernels = {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in kern.items()}
     lp = kern.get("pp_logprob_rows")
     logprob = None
@@ -254,7 +379,8 @@ def main():
         lp_ms = lp[0] / lp[1]
         gbs = (n_rows * V * 2 + n_rows * 16) / (lp_ms * 1e-3) / 1e9
         logprob = {"kernel": "pp_logprob_rows", "GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
-                   "rows": n_rows, "vocab": V, "avg_ms": round(lp_ms, 4)}
+                   "rows": n_rows, "vocab": V, "avg_ms": round(lp_ms, 4),
+                   "traffic": traffic_from_profile("pp_logprob_rows") if args.config == 1 else None}
 
     comp = None
     if not args.no_comparator:
