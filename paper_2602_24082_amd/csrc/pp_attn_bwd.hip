@@ -3,12 +3,13 @@
 // Three deterministic passes (no atomics):
 //
 //   bwd_prep   delta_i = dO_i . O_i  (fp32, [hq, sumT])
-//   bwd_dkdv   key-major: one workgroup = one 128-key tile of one kv-head, four
-//              waves of 32 keys each (K, V and the dK, dV accumulators live in
-//              registers).  It walks every query that sees the tile, for each
-//              query head of the kv-head's group, 64 queries per step, with the
-//              Q and dO tiles and the per-query LSE, delta and segment start
-//              DMA'd into a ring of LDS stages.  A prompt
+//   bwd_dkdv   key-major: one workgroup = one 128-key tile of one kv-head and
+//              eight waves; waves w and w+4 own keys 32*(w%4) .. +31 and take the
+//              two 32-query halves of each 64-query step (two waves per SIMD).
+//              It walks every query that sees the tile, for each query head of
+//              the kv-head's group, with the Q and dO tiles and the per-query
+//              LSE, delta and segment start DMA'd into two LDS stages; K and V
+//              stay in LDS.  A prompt
 //              key tile is visited by the prompt's later queries AND by every
 //              response's queries, so the shared prompt's dK/dV gather all K
 //              responses' contributions in one place.  Per step (S = Q K^T,
@@ -99,11 +100,28 @@ struct DkdvStage {
   int spare[KBM];  // receives the fourth wave's info DMA (keeps per-wave counts equal)
 };
 
-template <int D, int NS, typename TO>
-__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
-  using Dma = TileDma<D, KBM / 4>;
-  constexpr int PER_STEP = 2 * Dma::N + 1;  // DMA instructions per wave per step
-  __shared__ __attribute__((aligned(1024))) DkdvStage<D> st[NS];
+// Waves w and w+4 own the same 32 keys and take the
+// two 32-query halves of every 64-query step, so each SIMD runs two waves.  K
+// and V stay in LDS for the whole workgroup (B operands read by row), which
+// keeps a wave within 256 registers; the two halves' dK/dV partials are added
+// through LDS at the end.
+template <int D>
+struct DkdvSmem {
+  __bf16 k[KBN * D];
+  __bf16 v[KBN * D];
+  union {
+    DkdvStage<D> st[2];
+    float red[4][32 * D];  // partial dK or dV of waves 4..7
+  };
+};
+
+template <int D, typename TO>
+__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
+  using Dma = TileDma<D, KBM / 8>;
+  using KvDma = TileDma<D, KBN / 8>;
+  constexpr int NS = 2;
+  constexpr int PER_STEP = 2 * Dma::N + 1;
+  __shared__ __attribute__((aligned(1024))) DkdvSmem<D> sm;
 
   const int item_idx = blockIdx.x / p.hkv;
   const int g = blockIdx.x % p.hkv;
@@ -115,35 +133,41 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   const int lane = tid & 63;
   const int ln = lane & 31;
   const int hf = lane >> 5;
+  const int kb = wave & 3;   // key block of this wave
+  const int qb = wave >> 2;  // query half of every step
 
-  // this lane's key (column of S = Q K^T)
-  const int j = it.k0 + wave * 32 + ln;
+  const int j = it.k0 + kb * 32 + ln;
   const bool k_in_tile = j < it.k_end;
-  const bool k_real = j < it.valid;
   const int64_t krow = (int64_t)(it.tok0 + j) * p.hkv + g;
   const unsigned jP = (unsigned)(j - it.P);
-
-  const int wk0 = it.k0 + wave * 32;
+  const int wk0 = it.k0 + kb * 32;
   const int wk1 = min(min(it.k_end, it.valid), wk0 + 32);
   const bool wave_live = wk0 < wk1;
-  const int qlim = min(it.q_end, it.valid);  // queries at or past this are not real
+  const int qlim = min(it.q_end, it.valid);
 
   const int nq = it.q_end - it.q_begin;
   const int nsteps = (nq + KBM - 1) / KBM;
   const int n_iter = nq > 0 ? G * nsteps : 0;
   const int64_t q_stride = (int64_t)p.hq * D;
+  const int64_t kv_stride = (int64_t)p.hkv * D;
 
-  bf16x8 kf[D / 16], vf[D / 16];
-#pragma unroll
-  for (int c = 0; c < D / 16; ++c) {
-    kf[c] = k_real ? *reinterpret_cast<const bf16x8*>(p.k + krow * D + 16 * c + 8 * hf) : bf16x8{};
-    vf[c] = k_real ? *reinterpret_cast<const bf16x8*>(p.v + krow * D + 16 * c + 8 * hf) : bf16x8{};
+  // K and V of the tile, once (rows past the real keys repeat the last one)
+  {
+    KvDma kd;
+    kd.init(wave * (KBN / 8), kv_stride, lane);
+    const int rows = max(1, min(KBN, it.valid - it.k0));
+    const __bf16* kb0 = p.k + ((int64_t)(it.tok0 + min(it.k0, it.valid - 1)) * p.hkv + g) * D;
+    const __bf16* vb0 = p.v + ((int64_t)(it.tok0 + min(it.k0, it.valid - 1)) * p.hkv + g) * D;
+    if (it.valid > 0) {
+      kd.issue(sm.k, kb0, rows);
+      kd.issue(sm.v, vb0, rows);
+    }
   }
 
   Dma dma;
-  dma.init(wave * (KBM / 4), q_stride, lane);
+  dma.init(wave * (KBM / 8), q_stride, lane);
   auto issue = [&](int n) {
-    DkdvStage<D>& sg = st[n % NS];
+    DkdvStage<D>& sg = sm.st[n % NS];
     const int hh = n / nsteps, stp = n - hh * nsteps;
     const int head = g * G + hh;
     const int qs = it.q_begin + stp * KBM;
@@ -157,9 +181,7 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     else if (wave == 2) dma_dword(sg.seg_lo, p.seg_lo + tq);
     else dma_dword(sg.spare, p.seg_lo + tq);
   };
-#pragma unroll
-  for (int n = 0; n < NS - 1; ++n)
-    if (n < n_iter) issue(n);
+  if (n_iter > 0) issue(0);
 
   f32x16 acc_dk[D / 32], acc_dv[D / 32];
 #pragma unroll
@@ -169,87 +191,85 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   }
 
   for (int n = 0; n < n_iter; ++n) {
-    wait_tile<NS, PER_STEP>(n, n_iter);
-    __syncthreads();  // step n landed; the stage of step n-1 is free
-    if (n + NS - 1 < n_iter) issue(n + NS - 1);
+    wait_tile<NS, PER_STEP>(n, n_iter);  // the K/V tile (issued first) has landed as well
+    __syncthreads();
+    if (n + 1 < n_iter) issue(n + 1);
     if (!wave_live) continue;
-    const DkdvStage<D>& sg = st[n % NS];
+    const DkdvStage<D>& sg = sm.st[n % NS];
     const int qs = it.q_begin + (n % nsteps) * KBM;
+    const int qb0 = qs + qb * 32;
+    if (qb0 >= qlim) continue;
+    if (min(qb0 + 31, qlim - 1) < wk0) continue;
+
+    f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      // a block with no real query, or whose last real query precedes every key
-      // of the wave, has no visible pair
-      const int qb0 = qs + qb * 32;
-      if (qb0 >= qlim) continue;
-      if (min(qb0 + 31, qlim - 1) < wk0) continue;
-      // operands of the first two products (16-byte row reads)
-      bf16x8 aq[D / 16], ad[D / 16];
+    for (int c = 0; c < D / 16; ++c) {
+      s = mfma32(lds_row8<D>(sg.q, qb * 32 + ln, 2 * c + hf), lds_row8<D>(sm.k, kb * 32 + ln, 2 * c + hf), s);
+      dp = mfma32(lds_row8<D>(sg.dout, qb * 32 + ln, 2 * c + hf), lds_row8<D>(sm.v, kb * 32 + ln, 2 * c + hf), dp);
+    }
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        aq[c] = lds_row8<D>(sg.q, qb * 32 + ln, 2 * c + hf);
-        ad[c] = lds_row8<D>(sg.dout, qb * 32 + ln, 2 * c + hf);
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int il = qb * 32 + 8 * r4 + 4 * hf;
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sg.lse[il]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sg.delta[il]);
+      typedef int i32x4 __attribute__((ext_vector_type(4)));
+      const i32x4 o4 = *reinterpret_cast<const i32x4*>(&sg.seg_lo[il]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * r4 + e;
+        const int qi = qs + il + e;
+        const unsigned hole = o4[e] > it.P ? (unsigned)(o4[e] - it.P) : 0u;
+        const bool vis = (j <= qi) & (qi < qlim) & (jP >= hole);
+        const float ex = fast_exp2(fmaf(s[r], p.scale_log2, -l4[e] * kLog2e));
+        const float pr = vis ? ex : 0.f;
+        s[r] = pr;
+        dp[r] = pr * (dp[r] - d4[e]);
       }
-      f32x16 s = f32x16{}, dp = f32x16{};
+    }
+    const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
+    const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) {
-        s = mfma32(aq[c], kf[c], s);
-        dp = mfma32(ad[c], vf[c], dp);
-      }
-      // transposed operands of the last two products, requested before the
-      // softmax arithmetic so their latency hides behind it
-      bf16x8 tdo[D / 32][2], tq[D / 32][2];
-#pragma unroll
-      for (int m = 0; m < D / 32; ++m)
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-          tdo[m][h2] = lds_tr8<D>(sg.dout, qb * 32 + 16 * h2, 32 * m, lane);
-          tq[m][h2] = lds_tr8<D>(sg.q, qb * 32 + 16 * h2, 32 * m, lane);
-        }
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int il = qb * 32 + 8 * r4 + 4 * hf;  // rows il .. il+3 of this register group
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sg.lse[il]);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sg.delta[il]);
-        typedef int i32x4 __attribute__((ext_vector_type(4)));
-        const i32x4 o4 = *reinterpret_cast<const i32x4*>(&sg.seg_lo[il]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * r4 + e;
-          const int qi = qs + il + e;
-          const unsigned hole = o4[e] > it.P ? (unsigned)(o4[e] - it.P) : 0u;
-          const bool vis = (j <= qi) & (qi < qlim) & (jP >= hole);
-          const float ex = fast_exp2(fmaf(s[r], p.scale_log2, -l4[e] * kLog2e));
-          const float pr = vis ? ex : 0.f;
-          s[r] = pr;
-          dp[r] = pr * (dp[r] - d4[e]);
-        }
-      }
-      const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
-      const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
-#pragma unroll
-      for (int m = 0; m < D / 32; ++m) {
-        acc_dv[m] = mfma32(tdo[m][0], pb0, acc_dv[m]);
-        acc_dk[m] = mfma32(tq[m][0], db0, acc_dk[m]);
-        acc_dv[m] = mfma32(tdo[m][1], pb1, acc_dv[m]);
-        acc_dk[m] = mfma32(tq[m][1], db1, acc_dk[m]);
-      }
+    for (int m = 0; m < D / 32; ++m) {
+      acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
+      acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32, 32 * m, lane), db0, acc_dk[m]);
+      acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
+      acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
     }
   }
 
-  if (!k_in_tile) return;
+  wait_vmem<0>();  // a tile of padding keys has no steps: its K/V DMA is still owed
+  // add the second query half's partials into the first half's waves: first dK, then dV
+  float* red = sm.red[kb];
   TO* dkrow = p.dk + krow * D;
   TO* dvrow = p.dv + krow * D;
 #pragma unroll
-  for (int m = 0; m < D / 32; ++m)
+  for (int pass = 0; pass < 2; ++pass) {
+    __syncthreads();  // stages (pass 0) or the previous pass's buffer are free
+    if (qb == 1) {
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int d0 = 32 * m + 8 * r4 + 4 * hf;
-      f32x4 kv = {acc_dk[m][4 * r4] * p.scale, acc_dk[m][4 * r4 + 1] * p.scale,
-                  acc_dk[m][4 * r4 + 2] * p.scale, acc_dk[m][4 * r4 + 3] * p.scale};
-      f32x4 vv = {acc_dv[m][4 * r4], acc_dv[m][4 * r4 + 1], acc_dv[m][4 * r4 + 2], acc_dv[m][4 * r4 + 3]};
-      store4<TO>(dkrow + d0, kv);
-      store4<TO>(dvrow + d0, vv);
+      for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[(m * 16 + r) * 64 + lane] = pass == 0 ? acc_dk[m][r] : acc_dv[m][r];
     }
+    __syncthreads();
+    if (qb == 0 && k_in_tile) {
+      const float sc = pass == 0 ? p.scale : 1.f;
+      TO* dst = pass == 0 ? dkrow : dvrow;
+#pragma unroll
+      for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          f32x4 v4;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * r4 + e;
+            const float a = pass == 0 ? acc_dk[m][r] : acc_dv[m][r];
+            v4[e] = (a + red[(m * 16 + r) * 64 + lane]) * sc;
+          }
+          store4<TO>(dst + 32 * m + 8 * r4 + 4 * hf, v4);
+        }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -411,8 +431,8 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dkdv", s);
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, kDkdvStages, TO>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(256),
-                       0, s, p);
+    hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(512), 0, s,
+                       p);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -33,9 +33,6 @@ namespace pp {
 #ifndef PP_DQ_STAGES
 #define PP_DQ_STAGES 2
 #endif
-#ifndef PP_DKDV_STAGES
-#define PP_DKDV_STAGES 2
-#endif
 #ifndef PP_FWD_BLOCK_N
 #define PP_FWD_BLOCK_N 64
 #endif
@@ -45,17 +42,16 @@ namespace pp {
 
 // Tile sizes of the kernels (rows of the flat token axis).  Each wave of the
 // forward and dQ kernels owns 32 queries; each wave of the dK/dV kernel owns
-// 32 keys.
+// 32 keys and half of every 64-query step.
 constexpr int kFwdWaves = PP_FWD_WAVES;
 constexpr int kFwdStages = PP_FWD_STAGES;
 constexpr int kDqWaves = PP_DQ_WAVES;
 constexpr int kDqStages = PP_DQ_STAGES;
-constexpr int kDkdvStages = PP_DKDV_STAGES;
 constexpr int kFwdBlockM = 32 * kFwdWaves;  // queries per forward workgroup
 constexpr int kFwdBlockN = PP_FWD_BLOCK_N;  // keys per forward k-tile (32 or 64)
 constexpr int kDqBlockM = 32 * kDqWaves;    // queries per dQ workgroup
 constexpr int kDqBlockN = PP_DQ_BLOCK_N;    // keys per dQ k-tile (32 or 64)
-constexpr int kBwdBlockN = 128;             // keys per dK/dV workgroup (4 waves x 32)
+constexpr int kBwdBlockN = 128;             // keys per dK/dV workgroup (8 waves: 4 key blocks x 2)
 constexpr int kBwdBlockM = 64;              // queries per dK/dV inner step
 
 // One query tile: queries [q0, q_end) of the row starting at flat index tok0.
