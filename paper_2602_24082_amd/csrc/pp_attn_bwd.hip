@@ -125,11 +125,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
 
   const int item_idx = blockIdx.x / p.hkv;
   const int g = blockIdx.x % p.hkv;
-  const KTileItem it = p.kv_items[item_idx];
+  const KTileItem it = load_uniform(p.kv_items + item_idx);
   const int G = p.hq / p.hkv;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const int ln = lane & 31;
   const int hf = lane >> 5;
@@ -287,12 +287,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
-  const QTileItem it = p.dq_items[item_idx];
+  const QTileItem it = load_uniform(p.dq_items + item_idx);
   const int G = p.hq / p.hkv;
   const int g = head / G;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const int ln = lane & 31;
   const int hf = lane >> 5;
@@ -318,10 +318,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
   const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
   const int kv_lim = it.valid;
   const int n_tiles = it.kt_cnt;
+  const int32_t* ktiles = p.dq_ktiles + it.kt_off;
   Dma dma;
   dma.init(wave * RPW, kv_stride, lane);
   auto issue = [&](int t) {
-    const int k0 = p.dq_ktiles[it.kt_off + t];
+    const int k0 = tile_k0(scalar_load(ktiles + t));
     const int rows = min(QBN, kv_lim - k0);
     dma.issue(sKV[t % NS][0], kbase + k0 * kv_stride, rows);
     dma.issue(sKV[t % NS][1], vbase + k0 * kv_stride, rows);
@@ -334,22 +335,17 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
 #pragma unroll
   for (int m = 0; m < D / 32; ++m) acc[m] = f32x16{};
 
-  const bool wave_live = it.q0 + wave * 32 < it.q_end;
-
   for (int t = 0; t < n_tiles; ++t) {
-    const int k0 = p.dq_ktiles[it.kt_off + t];
+    const int32_t e = scalar_load(ktiles + t);
+    const int k0 = tile_k0(e);
+    const int cls = tile_wave_class(e, wave);
     wait_tile<NS, 2 * Dma::N>(t, n_tiles);
     __syncthreads();
     if (t + NS - 1 < n_tiles) issue(t + NS - 1);
-    if (!wave_live) continue;
+    if (cls == kWaveSkip) continue;
+    const bool need_mask = cls == kWaveMasked;
     const __bf16* sK = sKV[t % NS][0];
     const __bf16* sV = sKV[t % NS][1];
-
-    const int k_last = k0 + QBN - 1;
-    const bool lane_any = in_tile && hi >= k0 && (k0 < it.P || max(k0, lo) <= min(hi, k_last));
-    const bool lane_all = !in_tile || (k_last <= hi && (k0 + QBN <= it.P || k0 >= lo));
-    if (!__any(lane_any)) continue;
-    const bool need_mask = !__all(lane_all);
 
     f32x16 s[QKB], dp[QKB];
 #pragma unroll

@@ -10,8 +10,9 @@
 //     stages, NS-1 tiles ahead of the one being computed: one barrier per tile;
 //   * S^T = K Q^T on v_mfma_f32_32x32x16_bf16: lane l owns query l%32, so the
 //     softmax row statistics stay in the lane (one cross-half exchange);
-//   * the mask is evaluated only when the tile is not fully visible to the
-//     wave: visible(i, j) = j <= hi_i && j is not in [P, lo_i);
+//   * each list entry carries, per wave, whether the wave's 32 x BN block of
+//     pairs is invisible (skipped), fully visible, or mixed; only mixed blocks
+//     evaluate the mask visible(i, j) = j <= hi_i && j is not in [P, lo_i);
 //   * base-2 online softmax with scale*log2(e) folded in; the running maximum
 //     is only raised when a tile exceeds it by more than 2^8, so most tiles
 //     skip the rescale of O;
@@ -56,12 +57,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
-  const QTileItem it = p.items[item_idx];
+  const QTileItem it = load_uniform(p.items + item_idx);
   const int G = p.hq / p.hkv;
   const int g = head / G;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const int ln = lane & 31;
   const int hf = lane >> 5;
@@ -86,10 +87,13 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
   const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
   const int kv_lim = it.valid;
   const int n_tiles = it.kt_cnt;
+  // the tile list is wave-uniform: keep its address in scalar registers so the
+  // per-tile offsets come through the scalar cache
+  const int32_t* ktiles = p.ktiles + it.kt_off;
   Dma dma;
   dma.init(wave * RPW, kv_stride, lane);
   auto issue = [&](int t) {
-    const int k0 = p.ktiles[it.kt_off + t];
+    const int k0 = tile_k0(scalar_load(ktiles + t));
     const int rows = min(BN, kv_lim - k0);
     dma.issue(sKV[t % NS][0], kbase + k0 * kv_stride, rows);
     dma.issue(sKV[t % NS][1], vbase + k0 * kv_stride, rows);
@@ -104,23 +108,19 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
   float m_ref = kNegInf;  // reference maximum, scaled log2 units
   float l_run = 0.f;      // this lane's partial softmax denominator
 
-  const bool wave_live = it.q0 + wave * 32 < it.q_end;
   const float c2 = p.scale_log2;
 
   for (int t = 0; t < n_tiles; ++t) {
-    const int k0 = p.ktiles[it.kt_off + t];
+    const int32_t e = scalar_load(ktiles + t);
+    const int k0 = tile_k0(e);
+    const int cls = tile_wave_class(e, wave);
     wait_tile<NS, 2 * Dma::N>(t, n_tiles);
     __syncthreads();  // tile t landed for every wave; the stage of tile t-1 is free
     if (t + NS - 1 < n_tiles) issue(t + NS - 1);
-    if (!wave_live) continue;
+    if (cls == kWaveSkip) continue;
+    const bool need_mask = cls == kWaveMasked;
     const __bf16* sK = sKV[t % NS][0];
     const __bf16* sV = sKV[t % NS][1];
-
-    const int k_last = k0 + BN - 1;
-    const bool lane_any = in_tile && hi >= k0 && (k0 < it.P || max(k0, lo) <= min(hi, k_last));
-    const bool lane_all = !in_tile || (k_last <= hi && (k0 + BN <= it.P || k0 >= lo));
-    if (!__any(lane_any)) continue;
-    const bool need_mask = !__all(lane_all);
 
     // ---- S^T = K Q^T, one 32x32 block per 32 keys
     f32x16 s[KB];
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
     const bool raise = mx > m_ref + kRescaleSlack;
-    if (__any(raise)) {
+    if (wave_any(raise)) {
       const float m_new = raise ? mx : m_ref;
       // a lane that has seen no visible key yet has O = 0 and l = 0 (its m_ref
       // is -inf, and m_new may be -inf too): scale by 0 rather than exp2(nan)
@@ -162,16 +162,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
       m_ref = m_new;
     }
     const float mref = (m_ref == kNegInf) ? 0.f : m_ref;
-    float psum = 0.f;
+    float ps[2] = {0.f, 0.f};  // two partial sums: half the dependent-add chain
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = fast_exp2(fmaf(s[kb][r], c2, -mref));
-        s[kb][r] = e;
-        psum += e;
+        s[kb][r] = fast_exp2(fmaf(s[kb][r], c2, -mref));
+        ps[r & 1] += s[kb][r];
       }
-    l_run += psum;
+    l_run += ps[0] + ps[1];
 
     // ---- O^T += V^T P^T over 16-key chunks
     bf16x8 pb[2 * KB];

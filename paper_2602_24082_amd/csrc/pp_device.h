@@ -95,6 +95,20 @@ __device__ __forceinline__ bf16x8 acc_half_to_bf16(const f32x16& acc, int s) {
 // ---------------------------------------------------------------------------
 
 typedef __attribute__((address_space(3))) void lds_void;
+
+// One global_load_lds_dwordx4: lane l's 16 bytes at `src` land at LDS byte
+// address `lds_dst` (wave-uniform, passed through M0) + 16*l.  Every kernel
+// waits for these explicitly (wait_vmem / wait_tile) before the barrier that
+// publishes a stage, and reads a stage only after that barrier.
+__device__ __forceinline__ void lds_dma16(const void* src, const void* lds_dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_dst, 16, 0, 0);
+}
+
+// One 4-byte element per lane into LDS (lane l -> lds + 4*l): the per-query
+// scalars of a 64-query tile.
+__device__ __forceinline__ void dma_dword(void* lds, const void* src) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds, 4, 0, 0);
+}
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 template <int D>
@@ -135,24 +149,16 @@ struct TileDma {
     if (rows_valid >= row0 + N * RPI) {
 #pragma unroll
       for (int i = 0; i < N; ++i)
-        __builtin_amdgcn_global_load_lds((const void*)(src + off[i]),
-                                         (lds_void*)(lds_tile + (row0 + i * RPI) * D), 16, 0, 0);
+        lds_dma16(src + off[i], lds_tile + (row0 + i * RPI) * D);
     } else {
 #pragma unroll
       for (int i = 0; i < N; ++i) {
         const int rs = min(row_of(i), rows_valid - 1);
-        __builtin_amdgcn_global_load_lds((const void*)(src + rs * stride + chunk8_of(i)),
-                                         (lds_void*)(lds_tile + (row0 + i * RPI) * D), 16, 0, 0);
+        lds_dma16(src + rs * stride + chunk8_of(i), lds_tile + (row0 + i * RPI) * D);
       }
     }
   }
 };
-
-// One 4-byte element per lane into LDS (lane l -> lds + 4*l): the per-query
-// scalars of a 64-query tile.
-__device__ __forceinline__ void dma_dword(void* lds, const void* src) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds, 4, 0, 0);
-}
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
 // vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).
@@ -220,6 +226,30 @@ __device__ __forceinline__ float wave_max(float x) {
 __device__ __forceinline__ float wave_sum(float x) {
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
   return x;
+}
+
+// Wave-wide any of a lane predicate, as a value the compiler knows is uniform
+// (so a branch on it does not make a loop divergent).
+__device__ __forceinline__ bool wave_any(bool x) { return __builtin_amdgcn_readfirstlane(__any(x)) != 0; }
+
+// A plan record read so that the compiler keeps every field in scalar
+// registers (the record is the same for the whole workgroup).
+template <typename Item>
+__device__ __forceinline__ Item load_uniform(const Item* p) {
+  static_assert(sizeof(Item) % 4 == 0, "plan records are made of 32-bit fields");
+  Item out;
+  const int32_t* src = reinterpret_cast<const int32_t*>(p);
+  int32_t* dst = reinterpret_cast<int32_t*>(&out);
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(Item) / 4); ++i) dst[i] = __builtin_amdgcn_readfirstlane(src[i]);
+  return out;
+}
+
+// A read-only 32-bit value at a wave-uniform address, fetched with a scalar
+// load (through the constant address space) instead of a vector load whose
+// latency the wave would otherwise wait out in full.
+__device__ __forceinline__ int32_t scalar_load(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)p;
 }
 
 // Maps a linear workgroup index to (item, head).  Workgroups are dispatched to

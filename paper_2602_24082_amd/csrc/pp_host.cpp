@@ -113,6 +113,15 @@ pp_status check_heads(int hq, int hkv, int d) {
   return PP_OK;
 }
 
+// The attention plans address keys within a row with 24 bits.
+pp_status check_row_tokens(const Batch& bt) {
+  for (int b = 0; b < bt.B; ++b)
+    if (bt.rows[b].T >= kMaxRowTokens)
+      return fail(PP_ERR_UNSUPPORTED, "row %d has %d tokens; attention rows are limited to %d", b,
+                  bt.rows[b].T, kMaxRowTokens - 1);
+  return PP_OK;
+}
+
 pp_status check_dtype(pp_dtype t) {
   if (t != PP_BF16 && t != PP_FP32) return fail(PP_ERR_INVALID_ARGUMENT, "unknown dtype %d", (int)t);
   return PP_OK;
@@ -220,7 +229,20 @@ void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
       const int32_t kmax = std::min(it.q_end, r.valid);
       for (int32_t k0 = 0; k0 < kmax; k0 += BN) {
         const int32_t k1 = std::min(r.T, k0 + BN);
-        if (visible_pairs(r, q0, it.q_end, k0, k1) > 0) out->ktiles.push_back(k0);
+        if (visible_pairs(r, q0, it.q_end, k0, k1) == 0) continue;
+        uint32_t e = (uint32_t)k0;
+        for (int w = 0; w * 32 < BM; ++w) {
+          const int32_t qa = q0 + 32 * w, qb = std::min(it.q_end, qa + 32);
+          int cls = kWaveSkip;
+          if (qa < qb) {
+            const int64_t n = visible_pairs(r, qa, qb, k0, k1);
+            // a key tile cut short by the row's end leaves lanes without a key: masked
+            if (n == (int64_t)(qb - qa) * BN) cls = kWaveFull;
+            else if (n > 0) cls = kWaveMasked;
+          }
+          e |= (uint32_t)cls << (kTileK0Bits + 2 * w);
+        }
+        out->ktiles.push_back((int32_t)e);
       }
       it.kt_cnt = (int32_t)out->ktiles.size() - it.kt_off;
       out->items.push_back(it);
@@ -611,6 +633,7 @@ pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, in
   if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (fwd || bwd) {
     st = check_heads(hq, hkv, head_dim);
+    if (st == PP_OK) st = check_row_tokens(bt);
     if (st != PP_OK) return st;
   }
   if (fwd) {
@@ -642,6 +665,7 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_row_tokens(bt)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
@@ -701,6 +725,7 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_row_tokens(bt)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
