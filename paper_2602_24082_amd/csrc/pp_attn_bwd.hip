@@ -47,7 +47,7 @@ struct BwdParams {
   TO* dv;
   float* delta;
   const QTileItem* dq_items;
-  const int32_t* dq_ktiles;
+  const KTileEntry* dq_ktiles;
   const KTileItem* kv_items;
   const int32_t* seg_lo;
   int hq, hkv, sumT;
@@ -318,11 +318,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
   const __bf16* vbase = p.v + ((int64_t)it.tok0 * p.hkv + g) * D;
   const int kv_lim = it.valid;
   const int n_tiles = it.kt_cnt;
-  const int32_t* ktiles = p.dq_ktiles + it.kt_off;
+  const KTileEntry* ktiles = p.dq_ktiles + it.kt_off;
   Dma dma;
   dma.init(wave * RPW, kv_stride, lane);
   auto issue = [&](int t) {
-    const int k0 = tile_k0(scalar_load(ktiles + t));
+    const int k0 = scalar_load(&ktiles[t].k0);
     const int rows = min(QBN, kv_lim - k0);
     dma.issue(sKV[t % NS][0], kbase + k0 * kv_stride, rows);
     dma.issue(sKV[t % NS][1], vbase + k0 * kv_stride, rows);
@@ -336,9 +336,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
   for (int m = 0; m < D / 32; ++m) acc[m] = f32x16{};
 
   for (int t = 0; t < n_tiles; ++t) {
-    const int32_t e = scalar_load(ktiles + t);
-    const int k0 = tile_k0(e);
-    const int cls = tile_wave_class(e, wave);
+    const KTileEntry e = load_uniform(ktiles + t);
+    const int k0 = e.k0;
+    const int cls = tile_wave_class(e.cls, wave);
     wait_tile<NS, 2 * Dma::N>(t, n_tiles);
     __syncthreads();
     if (t + NS - 1 < n_tiles) issue(t + NS - 1);

@@ -42,7 +42,7 @@ struct FwdParams {
   TO* o;
   float* lse;
   const QTileItem* items;
-  const int32_t* ktiles;
+  const KTileEntry* ktiles;
   const int32_t* seg_lo;
   int hq, hkv, sumT;
   float scale;
@@ -89,11 +89,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
   const int n_tiles = it.kt_cnt;
   // the tile list is wave-uniform: keep its address in scalar registers so the
   // per-tile offsets come through the scalar cache
-  const int32_t* ktiles = p.ktiles + it.kt_off;
+  const KTileEntry* ktiles = p.ktiles + it.kt_off;
   Dma dma;
   dma.init(wave * RPW, kv_stride, lane);
   auto issue = [&](int t) {
-    const int k0 = tile_k0(scalar_load(ktiles + t));
+    const int k0 = scalar_load(&ktiles[t].k0);
     const int rows = min(BN, kv_lim - k0);
     dma.issue(sKV[t % NS][0], kbase + k0 * kv_stride, rows);
     dma.issue(sKV[t % NS][1], vbase + k0 * kv_stride, rows);
@@ -111,9 +111,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
   const float c2 = p.scale_log2;
 
   for (int t = 0; t < n_tiles; ++t) {
-    const int32_t e = scalar_load(ktiles + t);
-    const int k0 = tile_k0(e);
-    const int cls = tile_wave_class(e, wave);
+    const KTileEntry e = load_uniform(ktiles + t);
+    const int k0 = e.k0;
+    const int cls = tile_wave_class(e.cls, wave);
     wait_tile<NS, 2 * Dma::N>(t, n_tiles);
     __syncthreads();  // tile t landed for every wave; the stage of tile t-1 is free
     if (t + NS - 1 < n_tiles) issue(t + NS - 1);
@@ -122,13 +122,29 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
     const __bf16* sK = sKV[t % NS][0];
     const __bf16* sV = sKV[t % NS][1];
 
-    // ---- S^T = K Q^T, one 32x32 block per 32 keys
+    // ---- S^T = K Q^T, one 32x32 block per 32 keys; the K fragments are read
+    // from LDS PD steps ahead of the MFMA that consumes them (the scheduling
+    // barriers keep the compiler from bunching the reads)
     f32x16 s[KB];
+    {
+      constexpr int NC = D / 16, NI = KB * NC, PD = 3;  // K fragments in flight
+      bf16x8 a[PD + 1];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      s[kb] = f32x16{};
+      for (int kb = 0; kb < KB; ++kb) s[kb] = f32x16{};
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) s[kb] = mfma32(lds_row8<D>(sK, kb * 32 + ln, 2 * c + hf), qf[c], s[kb]);
+      for (int n = 0; n < PD; ++n) a[n] = lds_row8<D>(sK, (n / NC) * 32 + ln, 2 * (n % NC) + hf);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) a[(n + PD) % (PD + 1)] = lds_row8<D>(sK, ((n + PD) / NC) * 32 + ln, 2 * ((n + PD) % NC) + hf);
+        s[n / NC] = mfma32(a[n % (PD + 1)], qf[n % NC], s[n / NC]);
+      }
+#pragma unroll
+      for (int n = 0; n < PD; ++n) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      }
     }
     if (need_mask) {
       const int jb = k0 + 4 * hf;

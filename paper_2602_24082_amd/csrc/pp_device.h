@@ -121,40 +121,41 @@ __device__ __forceinline__ int swz(int r) {
 // comes from `src + min(r, rows_valid - 1) * stride` (elements), so rows past
 // the valid range repeat the last valid row (finite data that the mask then
 // ignores).  NR * D * 2 must be a multiple of 1 KB.  The per-lane part of the
-// addresses is computed once (`init`); `issue` then only adds the tile base.
+// addresses is a 32-bit byte offset computed once (`init`); `issue` adds it to
+// the wave-uniform tile base, which the loads take from scalar registers.
 template <int D, int NR>
 struct TileDma {
   static constexpr int RPI = 1024 / (D * 2);  // rows per wave instruction
   static constexpr int CPR = D / 8;           // 16-byte chunks per row
   static constexpr int N = NR / RPI;          // instructions per call
   static_assert(NR % RPI == 0, "tile rows must fill whole wave loads");
-  int off[N];   // element offset of this lane's chunk in instruction i, full tile
-  int64_t stride;
+  uint32_t off[N];  // byte offset of this lane's chunk in instruction i, full tile
+  uint32_t stride_b;  // bytes between tile rows
   int row0;
   int lane;
 
-  // tile row and 8 * logical chunk that this lane fetches in instruction i
+  // tile row and 16-byte chunk (of the swizzled row) that this lane fetches in instruction i
   __device__ __forceinline__ int row_of(int i) const { return row0 + i * RPI + lane / CPR; }
-  __device__ __forceinline__ int chunk8_of(int i) const { return ((lane % CPR) ^ swz<D>(row_of(i))) << 3; }
+  __device__ __forceinline__ uint32_t chunk_b(int i) const { return (uint32_t)((lane % CPR) ^ swz<D>(row_of(i))) << 4; }
 
   __device__ __forceinline__ void init(int row0_, int64_t stride_, int lane_) {
     row0 = row0_;
-    stride = stride_;
+    stride_b = (uint32_t)(stride_ * 2);
     lane = lane_;
 #pragma unroll
-    for (int i = 0; i < N; ++i) off[i] = (int)(row_of(i) * stride) + chunk8_of(i);
+    for (int i = 0; i < N; ++i) off[i] = (uint32_t)row_of(i) * stride_b + chunk_b(i);
   }
 
   __device__ __forceinline__ void issue(__bf16* lds_tile, const __bf16* src, int rows_valid) const {
+    const char* base = reinterpret_cast<const char*>(src);
     if (rows_valid >= row0 + N * RPI) {
 #pragma unroll
-      for (int i = 0; i < N; ++i)
-        lds_dma16(src + off[i], lds_tile + (row0 + i * RPI) * D);
+      for (int i = 0; i < N; ++i) lds_dma16(base + off[i], lds_tile + (row0 + i * RPI) * D);
     } else {
 #pragma unroll
       for (int i = 0; i < N; ++i) {
-        const int rs = min(row_of(i), rows_valid - 1);
-        lds_dma16(src + rs * stride + chunk8_of(i), lds_tile + (row0 + i * RPI) * D);
+        const uint32_t rs = (uint32_t)min(row_of(i), rows_valid - 1);
+        lds_dma16(base + (rs * stride_b + chunk_b(i)), lds_tile + (row0 + i * RPI) * D);
       }
     }
   }
@@ -227,6 +228,10 @@ __device__ __forceinline__ float wave_sum(float x) {
   for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
   return x;
 }
+
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 
 // Wave-wide any of a lane predicate, as a value the compiler knows is uniform
 // (so a branch on it does not make a loop divergent).

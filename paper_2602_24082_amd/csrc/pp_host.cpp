@@ -113,15 +113,6 @@ pp_status check_heads(int hq, int hkv, int d) {
   return PP_OK;
 }
 
-// The attention plans address keys within a row with 24 bits.
-pp_status check_row_tokens(const Batch& bt) {
-  for (int b = 0; b < bt.B; ++b)
-    if (bt.rows[b].T >= kMaxRowTokens)
-      return fail(PP_ERR_UNSUPPORTED, "row %d has %d tokens; attention rows are limited to %d", b,
-                  bt.rows[b].T, kMaxRowTokens - 1);
-  return PP_OK;
-}
-
 pp_status check_dtype(pp_dtype t) {
   if (t != PP_BF16 && t != PP_FP32) return fail(PP_ERR_INVALID_ARGUMENT, "unknown dtype %d", (int)t);
   return PP_OK;
@@ -208,7 +199,7 @@ uint8_t classify_tile(const Row& r, int32_t q0, int32_t q1, int32_t k0, int32_t 
 
 struct QPlan {
   std::vector<QTileItem> items;
-  std::vector<int32_t> ktiles;
+  std::vector<KTileEntry> ktiles;
 };
 
 void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
@@ -230,7 +221,7 @@ void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
       for (int32_t k0 = 0; k0 < kmax; k0 += BN) {
         const int32_t k1 = std::min(r.T, k0 + BN);
         if (visible_pairs(r, q0, it.q_end, k0, k1) == 0) continue;
-        uint32_t e = (uint32_t)k0;
+        KTileEntry e{k0, 0u};
         for (int w = 0; w * 32 < BM; ++w) {
           const int32_t qa = q0 + 32 * w, qb = std::min(it.q_end, qa + 32);
           int cls = kWaveSkip;
@@ -240,9 +231,9 @@ void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
             if (n == (int64_t)(qb - qa) * BN) cls = kWaveFull;
             else if (n > 0) cls = kWaveMasked;
           }
-          e |= (uint32_t)cls << (kTileK0Bits + 2 * w);
+          e.cls |= (uint32_t)cls << (2 * w);
         }
-        out->ktiles.push_back((int32_t)e);
+        out->ktiles.push_back(e);
       }
       it.kt_cnt = (int32_t)out->ktiles.size() - it.kt_off;
       out->items.push_back(it);
@@ -460,7 +451,7 @@ void plan_fwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, FwdPlan* 
   p->lay = Layout();
   p->r_seg = p->lay.add(p->seg_lo.size() * 4);
   p->r_items = p->lay.add(p->q.items.size() * sizeof(QTileItem));
-  p->r_kt = p->lay.add(p->q.ktiles.size() * 4);
+  p->r_kt = p->lay.add(p->q.ktiles.size() * sizeof(KTileEntry));
   p->lay.meta_bytes = p->lay.total;
   if (dtype == PP_FP32) {
     p->cast.on = true;
@@ -486,7 +477,7 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
   p->lay = Layout();
   p->r_seg = p->lay.add(p->seg_lo.size() * 4);
   p->r_dq_items = p->lay.add(p->dq.items.size() * sizeof(QTileItem));
-  p->r_dq_kt = p->lay.add(p->dq.ktiles.size() * 4);
+  p->r_dq_kt = p->lay.add(p->dq.ktiles.size() * sizeof(KTileEntry));
   p->r_kv_items = p->lay.add(p->kv.size() * sizeof(KTileItem));
   p->lay.meta_bytes = p->lay.total;
   p->r_delta = p->lay.add((size_t)hq * bt.sumT * 4);
@@ -633,7 +624,6 @@ pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, in
   if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (fwd || bwd) {
     st = check_heads(hq, hkv, head_dim);
-    if (st == PP_OK) st = check_row_tokens(bt);
     if (st != PP_OK) return st;
   }
   if (fwd) {
@@ -665,7 +655,6 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
-  if ((st = check_row_tokens(bt)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
@@ -680,7 +669,7 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   MetaImage img;
   img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
   img.put(p.lay.regions[p.r_items], p.q.items.data(), p.q.items.size() * sizeof(QTileItem));
-  img.put(p.lay.regions[p.r_kt], p.q.ktiles.data(), p.q.ktiles.size() * 4);
+  img.put(p.lay.regions[p.r_kt], p.q.ktiles.data(), p.q.ktiles.size() * sizeof(KTileEntry));
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
   hipError_t e;
   if (p.cast.on) {
@@ -703,7 +692,7 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   a.o = o;
   a.lse = lse;
   a.items = (const QTileItem*)at(ws, p.lay, p.r_items);
-  a.ktiles = (const int32_t*)at(ws, p.lay, p.r_kt);
+  a.ktiles = (const KTileEntry*)at(ws, p.lay, p.r_kt);
   a.seg_lo = (const int32_t*)at(ws, p.lay, p.r_seg);
   a.n_items = (int)p.q.items.size();
   a.hq = hq;
@@ -725,7 +714,6 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
-  if ((st = check_row_tokens(bt)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
@@ -740,7 +728,7 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   MetaImage img;
   img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
   img.put(p.lay.regions[p.r_dq_items], p.dq.items.data(), p.dq.items.size() * sizeof(QTileItem));
-  img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * 4);
+  img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * sizeof(KTileEntry));
   img.put(p.lay.regions[p.r_kv_items], p.kv.data(), p.kv.size() * sizeof(KTileItem));
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
   hipError_t e;
@@ -773,7 +761,7 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   a.dv = dv;
   a.delta = (float*)at(ws, p.lay, p.r_delta);
   a.dq_items = (const QTileItem*)at(ws, p.lay, p.r_dq_items);
-  a.dq_ktiles = (const int32_t*)at(ws, p.lay, p.r_dq_kt);
+  a.dq_ktiles = (const KTileEntry*)at(ws, p.lay, p.r_dq_kt);
   a.n_dq_items = (int)p.dq.items.size();
   a.kv_items = (const KTileItem*)at(ws, p.lay, p.r_kv_items);
   a.n_kv_items = (int)p.kv.size();

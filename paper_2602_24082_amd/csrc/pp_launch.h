@@ -34,7 +34,7 @@ struct AttnFwdLaunch {
   void* o;
   float* lse;
   const QTileItem* items;
-  const int32_t* ktiles;
+  const KTileEntry* ktiles;
   const int32_t* seg_lo;
   int n_items;
   int hq, hkv, head_dim;
@@ -58,7 +58,7 @@ struct AttnBwdLaunch {
   void* dv;
   float* delta;              // [hq, sumT] scratch
   const QTileItem* dq_items;
-  const int32_t* dq_ktiles;
+  const KTileEntry* dq_ktiles;
   int n_dq_items;
   const KTileItem* kv_items;
   int n_kv_items;

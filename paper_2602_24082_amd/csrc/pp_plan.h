@@ -55,22 +55,21 @@ constexpr int kDqBlockN = PP_DQ_BLOCK_N;    // keys per dQ k-tile (32 or 64)
 constexpr int kBwdBlockN = 128;             // keys per dK/dV workgroup (8 waves: 4 key blocks x 2)
 constexpr int kBwdBlockM = 64;              // queries per dK/dV inner step
 
-// An entry of a query tile's key-tile list: the tile's first key (row-relative,
-// low 24 bits) and, per 32-query wave of the query tile, a 2-bit class of the
-// wave's block of pairs against the key tile, worked out exactly on the host:
+// An entry of a query tile's key-tile list: the tile's first key (row-relative)
+// and, per 32-query wave of the query tile, a 2-bit class of the wave's block
+// of pairs against the key tile, worked out exactly on the host:
 //   kWaveSkip   no pair of the block is visible (the wave sits the tile out);
 //   kWaveFull   every pair is visible (no mask);
 //   kWaveMasked some pairs are visible (the mask is evaluated per element).
-constexpr int kTileK0Bits = 24;
-constexpr int32_t kTileK0Mask = (1 << kTileK0Bits) - 1;
-constexpr int kMaxRowTokens = 1 << kTileK0Bits;  // rows must be shorter
+struct KTileEntry {
+  int32_t k0;
+  uint32_t cls;  // bits 2w, 2w+1: class of wave w
+};
 constexpr int kWaveSkip = 0, kWaveFull = 1, kWaveMasked = 2;
-static_assert(kFwdWaves <= 4 && kDqWaves <= 4, "2 class bits per wave in 8 bits");
+constexpr int kMaxClassWaves = 16;
+static_assert(kFwdWaves <= kMaxClassWaves && kDqWaves <= kMaxClassWaves, "2 class bits per wave");
 
-inline __host__ __device__ int32_t tile_k0(int32_t e) { return e & kTileK0Mask; }
-inline __host__ __device__ int tile_wave_class(int32_t e, int wave) {
-  return (int)(((uint32_t)e >> (kTileK0Bits + 2 * wave)) & 3u);
-}
+inline __host__ __device__ int tile_wave_class(uint32_t cls, int wave) { return (int)((cls >> (2 * wave)) & 3u); }
 
 // One query tile: queries [q0, q_end) of the row starting at flat index tok0.
 struct QTileItem {
