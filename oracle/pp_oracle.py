@@ -46,6 +46,10 @@ R9  Softmax scale 1/sqrt(d) unless given; q-head h uses kv-head floor(h/G).
 R10 Padding tokens: attention output, LSE and all gradients are 0; an empty
     response scores 0; rows with fewer than two responses are left out of the
     loss mean.
+R11 Log-prob backward: the gradient reaching the logits is that of
+    sum_{b,k} g_bk * seq_bk for given g = dL/dseq (the loss gradient); logit rows
+    that predict no response token get 0, and a label outside the vocabulary
+    makes its whole predicting row NaN (the forward makes the sum NaN).
 
 All floating-point work is numpy float64.  Parity of every function here is
 pinned by tests against closed forms, brute force on tiny inputs, finite
@@ -314,6 +318,40 @@ def seq_logprob(row_start, prompt_len, num_resp, resp_off, resp_len, logits, tok
                 s += lp
             seq[b, kk] = s
     return seq, tok
+
+
+def seq_logprob_grad(row_start, prompt_len, num_resp, resp_off, resp_len, logits, tokens, dseq):
+    """Gradient of sum_{b,k} dseq[b,k] * seq[b,k] with respect to the logits (R11).
+
+    seq is seq_logprob's per-response sum, so every response token contributes
+    dseq[b,k] * (onehot(label) - softmax(predicting row)) to the row that
+    predicts it: the last prompt row once per response (its first token), the
+    row before the token otherwise.  Rows that predict no response token get 0.
+    A label outside [0, V) makes the whole predicting row NaN.
+    """
+    logits = np.asarray(logits, dtype=np.float64)
+    tokens = np.asarray(tokens)
+    dseq = np.asarray(dseq, dtype=np.float64)
+    V = logits.shape[1]
+    grad = np.zeros_like(logits)
+    bad = np.zeros(logits.shape[0], dtype=bool)
+    for b in range(len(prompt_len)):
+        r0, T, P, offs, lens = _row_fields(row_start, prompt_len, num_resp, resp_off, resp_len, b)
+        for kk, (o, L) in enumerate(zip(offs, lens)):
+            g = float(dseq[b, kk])
+            for j in range(L):
+                t = o + j
+                src = r0 + ((P - 1) if j == 0 else (t - 1))
+                y = int(tokens[r0 + t])
+                if not (0 <= y < V):
+                    bad[src] = True
+                    continue
+                row = logits[src]
+                p = np.exp(row - logsumexp_row(row))
+                grad[src] -= g * p
+                grad[src, y] += g
+    grad[bad] = np.nan
+    return grad
 
 
 def logprob_rows_needed(prompt_len, num_resp, resp_len):
