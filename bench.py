@@ -382,6 +382,31 @@ def main():
                    "rows": n_rows, "vocab": V, "avg_ms": round(lp_ms, 4),
                    "traffic": traffic_from_profile("pp_logprob_rows") if args.config == 1 else None}
 
+    # log-prob backward (the next link of the DPO chain): timed on its own, the
+    # step above keeps to the forward hot path
+    dlogits = torch.empty_like(logits_pol)
+    _, _, dseq = pp.pp_dpo_loss(num_resp, seq_pol, seq_ref if with_ref else None, beta, ws=ws_loss)
+    for _ in range(2):
+        pp.pp_seq_logprob_bwd(pack, logits_pol, tokens, dseq, dlogits=dlogits, ws=ws_lp)
+    torch.cuda.synchronize()
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    for _ in range(max(3, args.steps // 2)):
+        pp.pp_seq_logprob_bwd(pack, logits_pol, tokens, dseq, dlogits=dlogits, ws=ws_lp)
+    torch.cuda.synchronize()
+    pp.pp_timing_enable(False)
+    kb = pp.pp_timing_get().get("pp_logprob_bwd")
+    logprob_bwd = None
+    if kb:
+        kb_ms = kb[0] / kb[1]
+        nbytes = n_rows * V * 2 + T * V * 2
+        gbs = nbytes / (kb_ms * 1e-3) / 1e9
+        logprob_bwd = {"kernel": "pp_logprob_bwd", "GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                       "algorithmic_bytes": nbytes, "avg_ms": round(kb_ms, 4),
+                       "bytes_rule": "needed logit rows read once + every dlogits row written once (bf16)",
+                       "traffic": traffic_from_profile("pp_logprob_bwd") if args.config == 1 else None}
+    del dlogits
+
     comp = None
     if not args.no_comparator:
         padded = wl.unpacked_padded(pack)
@@ -420,6 +445,7 @@ def main():
         "speedup_vs_padded": comp["speedup_vs_padded"] if comp else None,
         "comparator": comp,
         "logprob": logprob,
+        "logprob_bwd": logprob_bwd,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,

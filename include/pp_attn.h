@@ -11,6 +11,7 @@
  *   pp_attn_fwd     masked attention forward over packed rows  (Sec. 3.2)
  *   pp_attn_bwd     its gradients dQ, dK, dV                   (Sec. 3.2)
  *   pp_seq_logprob  per-response summed token log-probs        (Sec. 2.1, Sec. 3.2)
+ *   pp_seq_logprob_bwd  their gradient with respect to the logits
  *   pp_dpo_loss     ranked-pair DPO / Bradley-Terry loss        (Sec. 2.1)
  *
  * Conventions shared by every entry point
@@ -92,7 +93,8 @@ typedef struct pp_pack_desc {
  * Any output pointer may be NULL.  dtype is the attention input dtype (fp32
  * inputs need room for their bf16 copies).  vocab is used only for logprob and
  * may be 0.  hq, hkv and head_dim are validated as for pp_attn_fwd when fwd or
- * bwd is requested.  loss is the workspace of pp_dpo_loss for this batch's B. */
+ * bwd is requested.  logprob serves both pp_seq_logprob and pp_seq_logprob_bwd.
+ * loss is the workspace of pp_dpo_loss for this batch's B. */
 pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                             int vocab, size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss);
 
@@ -143,6 +145,22 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
 pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
                          const void* logits, const int32_t* tokens, float* seq_logp,
                          float* tok_logp, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Backward of pp_seq_logprob: the gradient of sum_{b,k} dseq[b*K_max+k] *
+ * seq_logp[b*K_max+k] with respect to the logits (Sec. 2.1 scores; dseq is
+ * typically pp_dpo_loss's dlogp_pol).  Every response token adds
+ * dseq[b,k] * (onehot(label) - softmax(row)) to the logit row that predicts it
+ * (the same rows as pp_seq_logprob, so the last prompt row gathers the first
+ * token of every response); every other row of dlogits is written as 0.  A
+ * label outside [0, vocab) makes its predicting row NaN.
+ * logits (dev [sumT, vocab], logits_dtype), tokens (dev int32 [sumT]), dseq (dev
+ * float [B*K_max]); dlogits (dev [sumT, vocab], logits_dtype) is overwritten.
+ * Softmax and products are computed in fp32; bf16 outputs are rounded to
+ * nearest even.  ws_bytes >= pp_workspace_size's logprob.
+ * Errors: as pp_seq_logprob; PP_ERR_UNSUPPORTED when max_resp > 256. */
+pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                             const void* logits, const int32_t* tokens, const float* dseq,
+                             void* dlogits, void* ws, size_t ws_bytes, void* hip_stream);
 
 /* Ranked-pair DPO / Bradley-Terry loss (Sec. 2.1, extended to K > 2).
  * z_k = beta (logp_pol[b,k] - logp_ref[b,k]), or beta logp_pol[b,k] when

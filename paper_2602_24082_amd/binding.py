@@ -27,7 +27,7 @@ STATUS = {0: "PP_OK", 1: "PP_ERR_INVALID_ARGUMENT", 2: "PP_ERR_BAD_LAYOUT", 3: "
           4: "PP_ERR_WORKSPACE_TOO_SMALL", 5: "PP_ERR_HIP"}
 
 EXPORTED = [
-    "pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_dpo_loss",
+    "pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_seq_logprob_bwd", "pp_dpo_loss",
     "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
 ]
@@ -73,6 +73,7 @@ def lib() -> ctypes.CDLL:
     L.pp_attn_fwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, sz, P]
     L.pp_attn_bwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, P, P, P, P, sz, P]
     L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
+    L.pp_seq_logprob_bwd.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_dpo_loss.argtypes = [i32, i32, P, P, P, ctypes.c_float, P, P, P, P, sz, P]
     L.pp_pack_export.argtypes = [D, i, i, P, P, P, sz]
     L.pp_tile_class_len.argtypes = [D, i, i, ctypes.POINTER(sz)]
@@ -206,6 +207,26 @@ def pp_seq_logprob(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, want_
     _check(lib().pp_seq_logprob(h.ref, _dtype_code(logits), V, _ptr(logits), _ptr(tokens), _ptr(seq),
                                 _ptr(tok), _ptr(ws), ws.numel(), _stream(dev)))
     return (seq, tok) if want_tok else seq
+
+
+def pp_seq_logprob_bwd(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, dseq: torch.Tensor,
+                       dlogits=None, ws=None):
+    """Gradient of sum(dseq * seq_logp) w.r.t. the logits: [sumT, V] in the logits' dtype."""
+    V = logits.shape[1]
+    h = _DescHolder(pack)
+    dev = logits.device
+    if dlogits is None:
+        dlogits = torch.empty_like(logits)
+    if ws is None:
+        nb = pp_workspace_size(pack, vocab=V, fwd=False, bwd=False, logprob=True, loss=False)[2]
+        ws = _workspace(nb, dev)
+    if tokens.dtype != torch.int32:
+        raise TypeError("tokens must be int32")
+    if dseq.dtype != torch.float32 or not dseq.is_contiguous():
+        raise TypeError("dseq must be contiguous float32 [B, K_max]")
+    _check(lib().pp_seq_logprob_bwd(h.ref, _dtype_code(logits), V, _ptr(logits), _ptr(tokens), _ptr(dseq),
+                                    _ptr(dlogits), _ptr(ws), ws.numel(), _stream(dev)))
+    return dlogits
 
 
 def pp_dpo_loss(num_resp, logp_pol: torch.Tensor, logp_ref: Optional[torch.Tensor], beta: float,

@@ -287,13 +287,15 @@ void build_seg_lo(const Batch& bt, std::vector<int32_t>* out) {
 
 struct LPlan {
   std::vector<LogitRowItem> rows;
-  std::vector<int32_t> labels;
+  std::vector<int32_t> labels;     // flat position of each label token
+  std::vector<int32_t> label_out;  // its response's slot b * K_max + k
   std::vector<RespItem> resp;
 };
 
 void build_lplan(const Batch& bt, LPlan* out) {
   out->rows.clear();
   out->labels.clear();
+  out->label_out.clear();
   out->resp.clear();
   for (int b = 0; b < bt.B; ++b) {
     const Row& r = bt.rows[b];
@@ -305,7 +307,10 @@ void build_lplan(const Batch& bt, LPlan* out) {
       it.logit_row = (int64_t)r.tok0 + r.P - 1;
       it.label_off = (int32_t)out->labels.size();
       for (int k = 0; k < r.K; ++k)
-        if (r.len[k] > 0) out->labels.push_back(r.tok0 + r.off[k]);
+        if (r.len[k] > 0) {
+          out->labels.push_back(r.tok0 + r.off[k]);
+          out->label_out.push_back(b * bt.Kmax + k);
+        }
       it.label_cnt = (int32_t)out->labels.size() - it.label_off;
       out->rows.push_back(it);
       for (int k = 0; k < r.K; ++k) {
@@ -315,6 +320,7 @@ void build_lplan(const Batch& bt, LPlan* out) {
           e.label_off = (int32_t)out->labels.size();
           e.label_cnt = 1;
           out->labels.push_back(r.tok0 + r.off[k] + j);
+          out->label_out.push_back(b * bt.Kmax + k);
           out->rows.push_back(e);
         }
       }
@@ -490,18 +496,26 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
   }
 }
 
+// One workspace layout serves the log-prob forward and its backward: the
+// backward also stages each label's response slot and, per flat logit row, the
+// index of the gather record that reads it (-1 for rows that predict nothing).
 struct LogprobPlan {
   LPlan l;
+  std::vector<int32_t> row_item;
   Layout lay;
-  size_t r_rows, r_labels, r_resp, r_tok;
+  size_t r_rows, r_labels, r_resp, r_label_out, r_row_item, r_tok;
 };
 
 void plan_logprob(const Batch& bt, LogprobPlan* p) {
   build_lplan(bt, &p->l);
+  p->row_item.assign(bt.sumT, -1);
+  for (size_t i = 0; i < p->l.rows.size(); ++i) p->row_item[p->l.rows[i].logit_row] = (int32_t)i;
   p->lay = Layout();
   p->r_rows = p->lay.add(p->l.rows.size() * sizeof(LogitRowItem));
   p->r_labels = p->lay.add(p->l.labels.size() * 4);
   p->r_resp = p->lay.add(p->l.resp.size() * sizeof(RespItem));
+  p->r_label_out = p->lay.add(p->l.label_out.size() * 4);
+  p->r_row_item = p->lay.add(p->row_item.size() * 4);
   p->lay.meta_bytes = p->lay.total;
   p->r_tok = p->lay.add((size_t)bt.sumT * 4);
 }
@@ -817,6 +831,52 @@ pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vo
   a.dtype = logits_dtype == PP_FP32 ? kFP32 : kBF16;
   hipError_t e = launch_logprob(a, s);
   if (e != hipSuccess) return hip_fail(e, "logprob launch");
+  return PP_OK;
+}
+
+pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                             const void* logits, const int32_t* tokens, const float* dseq,
+                             void* dlogits, void* ws, size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_dtype(logits_dtype)) != PP_OK) return st;
+  if (vocab < 1) return fail(PP_ERR_INVALID_ARGUMENT, "vocab must be >= 1");
+  if ((st = check_logprob_layout(bt)) != PP_OK) return st;
+  if (bt.Kmax > kMaxRowLabels)
+    return fail(PP_ERR_UNSUPPORTED, "the log-prob backward takes at most %d responses per row (max_resp %d)",
+                kMaxRowLabels, bt.Kmax);
+  if (bt.sumT == 0) return PP_OK;
+  if (!logits || !tokens || !dlogits) return fail(PP_ERR_INVALID_ARGUMENT, "logits, tokens and dlogits must be non-NULL");
+  if (bt.Kmax > 0 && !dseq) return fail(PP_ERR_INVALID_ARGUMENT, "dseq is NULL");
+  LogprobPlan p;
+  plan_logprob(bt, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "logprob needs %zu workspace bytes, got %zu", p.lay.total,
+                ws_bytes);
+  if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  hipStream_t s = (hipStream_t)hip_stream;
+  MetaImage img;
+  img.put(p.lay.regions[p.r_rows], p.l.rows.data(), p.l.rows.size() * sizeof(LogitRowItem));
+  img.put(p.lay.regions[p.r_labels], p.l.labels.data(), p.l.labels.size() * 4);
+  img.put(p.lay.regions[p.r_resp], p.l.resp.data(), p.l.resp.size() * sizeof(RespItem));
+  img.put(p.lay.regions[p.r_label_out], p.l.label_out.data(), p.l.label_out.size() * 4);
+  img.put(p.lay.regions[p.r_row_item], p.row_item.data(), p.row_item.size() * 4);
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  LogprobBwdLaunch a{};
+  a.logits = logits;
+  a.tokens = tokens;
+  a.dseq = dseq;
+  a.dlogits = dlogits;
+  a.rows = (const LogitRowItem*)at(ws, p.lay, p.r_rows);
+  a.labels = (const int32_t*)at(ws, p.lay, p.r_labels);
+  a.label_out = (const int32_t*)at(ws, p.lay, p.r_label_out);
+  a.row_item = (const int32_t*)at(ws, p.lay, p.r_row_item);
+  a.vocab = vocab;
+  a.sumT = bt.sumT;
+  a.dtype = logits_dtype == PP_FP32 ? kFP32 : kBF16;
+  hipError_t e = launch_logprob_bwd(a, s);
+  if (e != hipSuccess) return hip_fail(e, "logprob backward launch");
   return PP_OK;
 }
 

@@ -86,6 +86,21 @@ struct LogprobLaunch {
 };
 hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s);
 
+struct LogprobBwdLaunch {
+  const void* logits;
+  const int32_t* tokens;
+  const float* dseq;          // [B * K_max] dL/dseq
+  void* dlogits;              // [sumT, vocab], logits dtype
+  const LogitRowItem* rows;
+  const int32_t* labels;      // flat token positions
+  const int32_t* label_out;   // response slot of each label
+  const int32_t* row_item;    // [sumT]: gather record of each logit row or -1
+  int vocab;
+  int sumT;
+  int dtype;
+};
+hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s);
+
 struct LossLaunch {
   const int32_t* num_resp;   // device copy [B]
   const float* pol;

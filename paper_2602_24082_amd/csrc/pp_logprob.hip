@@ -3,13 +3,17 @@
 // The DPO reward of Sec. 2.1 is built from sequence log-probabilities
 // log pi(y|x) = sum_t log softmax(logits_{t-1})[y_t].  In a packed row (Sec. 3.2)
 // the first token of every response is predicted by the last prompt position,
-// the others by the position before them.  Three kernels:
+// the others by the position before them.  Kernels:
 //
 //   fill_zero      tok[:] = 0                                  (HBM write, tiny)
 //   logprob_rows   one workgroup per needed logit row: one streaming pass over
 //                  the vocabulary for (max, sum exp), then the label logits
 //                  -> tok[label position] = logit[label] - logsumexp
 //                  (HBM-bound: reads each needed logit row once)
+//   logprob_bwd    one workgroup per flat logit row: the gradient of the
+//                  weighted response sums, -c softmax + label terms, zeros for
+//                  rows that predict nothing (HBM-bound: one read of the needed
+//                  rows, a cached re-read, one write of every row)
 //   segsum         one wave per (row, response) slot: fixed-order sum of the
 //                  response's token log-probs -> seq[b, k]
 //   pair_loss      one workgroup: z = beta (pol - ref), softplus over ranked
@@ -84,13 +88,12 @@ struct Vec16<float> {
   }
 };
 
+// ln sum_v exp(x[v]) of one logit row, for every thread of a kLpThreads
+// workgroup: one streaming pass of 16-byte loads (kLpUnroll in flight per
+// thread) keeping an online (max, sum) per thread, then a fixed-order
+// workgroup combine.
 template <typename T>
-__global__ __launch_bounds__(kLpThreads) void logprob_rows_kernel(
-    const T* __restrict__ logits, const int32_t* __restrict__ tokens,
-    const LogitRowItem* __restrict__ rows, const int32_t* __restrict__ labels,
-    float* __restrict__ tok, int vocab) {
-  const LogitRowItem it = rows[blockIdx.x];
-  const T* x = logits + it.logit_row * (int64_t)vocab;
+__device__ float row_logsumexp(const T* __restrict__ x, int vocab) {
   const int tid = threadIdx.x;
   MaxSum acc = {kNegInf, 0.f};
   constexpr int N = Vec16<T>::N;
@@ -159,11 +162,134 @@ __global__ __launch_bounds__(kLpThreads) void logprob_rows_kernel(
     s_lse = t.m + logf(t.s);
   }
   __syncthreads();
-  const float lse = s_lse;
-  for (int j = tid; j < it.label_cnt; j += kLpThreads) {
+  return s_lse;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kLpThreads) void logprob_rows_kernel(
+    const T* __restrict__ logits, const int32_t* __restrict__ tokens,
+    const LogitRowItem* __restrict__ rows, const int32_t* __restrict__ labels,
+    float* __restrict__ tok, int vocab) {
+  const LogitRowItem it = rows[blockIdx.x];
+  const T* x = logits + it.logit_row * (int64_t)vocab;
+  const float lse = row_logsumexp<T>(x, vocab);
+  for (int j = threadIdx.x; j < it.label_cnt; j += kLpThreads) {
     const int32_t pos = labels[it.label_off + j];
     const int32_t y = tokens[pos];
     tok[pos] = (y >= 0 && y < vocab) ? elem<T>(x, y) - lse : __builtin_nanf("");
+  }
+}
+
+// Packs floats into one 16-byte vector of T (bf16: round to nearest even).
+template <typename T>
+struct Pack16;
+template <>
+struct Pack16<__bf16> {
+  __device__ __forceinline__ static u32x4 pack(const float* f) {
+    typedef float f32x8 __attribute__((ext_vector_type(8)));
+    const f32x8 v = {f[0], f[1], f[2], f[3], f[4], f[5], f[6], f[7]};
+    return __builtin_bit_cast(u32x4, __builtin_convertvector(v, bf16x8));
+  }
+};
+template <>
+struct Pack16<float> {
+  __device__ __forceinline__ static u32x4 pack(const float* f) {
+    return u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]), __float_as_uint(f[3])};
+  }
+};
+
+// Log-prob backward: one workgroup per flat logit row r.  With c = the sum of
+// g over the labels that row r predicts,
+//   dlogits[r, v] = -c softmax(x_r)[v] + sum_{labels y = v} g,
+// the gradient of sum_bk g_bk seq_bk; rows that predict nothing get 0 and a
+// label outside the vocabulary makes its row NaN.  The row's logsumexp is
+// recomputed with one pass; a second pass re-reads the row (mostly from the
+// caches) and streams the gradient out.
+template <typename T>
+__global__ __launch_bounds__(kLpThreads) void logprob_bwd_kernel(LogprobBwdLaunch a) {
+  const int64_t r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int vocab = a.vocab;
+  T* out = reinterpret_cast<T*>(a.dlogits) + r * (int64_t)vocab;
+  constexpr int N = Vec16<T>::N;
+  const bool aligned = ((r * (int64_t)vocab * (int64_t)sizeof(T)) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.dlogits) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0;
+  const int nvec = aligned ? vocab / N : 0;
+  const int item = a.row_item[r];
+  if (item < 0) {
+    u32x4* ov = reinterpret_cast<u32x4*>(out);
+    for (int vi = tid; vi < nvec; vi += kLpThreads) __builtin_nontemporal_store(u32x4{0, 0, 0, 0}, ov + vi);
+    for (int64_t v = (int64_t)nvec * N + tid; v < vocab; v += kLpThreads) out[v] = (T)0.f;
+    return;
+  }
+  const LogitRowItem it = a.rows[item];
+  const T* x = reinterpret_cast<const T*>(a.logits) + r * (int64_t)vocab;
+  __shared__ int s_y[kMaxRowLabels];
+  __shared__ float s_g[kMaxRowLabels];
+  __shared__ float s_c;
+  __shared__ int s_bad;
+  const int cnt = it.label_cnt;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  for (int j = tid; j < cnt; j += kLpThreads) {
+    const int32_t y = a.tokens[a.labels[it.label_off + j]];
+    s_y[j] = y;
+    s_g[j] = a.dseq[a.label_out[it.label_off + j]];
+    if (y < 0 || y >= vocab) s_bad = 1;
+  }
+  const float lse = row_logsumexp<T>(x, vocab);  // its barriers publish s_y, s_g, s_bad
+  if (tid == 0) {
+    float c = 0.f;
+    for (int j = 0; j < cnt; ++j) c += s_g[j];
+    s_c = c;
+  }
+  __syncthreads();
+  const float c = s_c;
+  const bool bad = s_bad != 0;
+  const float lse2 = lse * kLog2e;
+  // -c softmax for every element; the few label terms are added only to the
+  // vectors that hold a label
+  auto label_terms = [&](float* f, int v0, int n) {
+    for (int j = 0; j < cnt; ++j) {
+      const int d = s_y[j] - v0;
+      if ((unsigned)d < (unsigned)n) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) f[e] += (e == d) ? s_g[j] : 0.f;
+      }
+    }
+  };
+  const u32x4* xv = reinterpret_cast<const u32x4*>(x);
+  u32x4* ov = reinterpret_cast<u32x4*>(out);
+  for (int base = 0; base < nvec; base += kLpThreads * kLpUnroll) {
+    u32x4 u[kLpUnroll];
+#pragma unroll
+    for (int j = 0; j < kLpUnroll; ++j) {
+      const int vi = base + j * kLpThreads + tid;
+      u[j] = vi < nvec ? xv[vi] : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int j = 0; j < kLpUnroll; ++j) {
+      const int vi = base + j * kLpThreads + tid;
+      if (vi < nvec) {
+        float f[N];
+        Vec16<T>::unpack(u[j], f);
+#pragma unroll
+        for (int e = 0; e < N; ++e) f[e] = -c * fast_exp2(fmaf(f[e], kLog2e, -lse2));
+        label_terms(f, vi * N, N);
+        if (bad) {
+#pragma unroll
+          for (int e = 0; e < N; ++e) f[e] = __builtin_nanf("");
+        }
+        __builtin_nontemporal_store(Pack16<T>::pack(f), ov + vi);
+      }
+    }
+  }
+  for (int64_t v = (int64_t)nvec * N + tid; v < vocab; v += kLpThreads) {
+    float f[N] = {};
+    f[0] = -c * fast_exp2(fmaf(elem<T>(x, v), kLog2e, -lse2));
+    label_terms(f, (int)v, 1);
+    out[v] = (T)(bad ? __builtin_nanf("") : f[0]);
   }
 }
 
@@ -265,6 +391,16 @@ hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s) {
     e = hipGetLastError();
   }
   return e;
+}
+
+hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s) {
+  if (a.sumT <= 0) return hipSuccess;
+  TimingScope t("pp_logprob_bwd", s);
+  if (a.dtype == kBF16)
+    hipLaunchKernelGGL(logprob_bwd_kernel<__bf16>, dim3(a.sumT), dim3(kLpThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(logprob_bwd_kernel<float>, dim3(a.sumT), dim3(kLpThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_loss(const LossLaunch& a, hipStream_t s) {

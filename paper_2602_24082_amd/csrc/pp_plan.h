@@ -102,6 +102,10 @@ struct LogitRowItem {
   int32_t label_cnt;  // number of labels predicted from this row
 };
 
+// Labels one logit row can predict in the log-prob backward (the last prompt
+// row predicts the first token of each of its K responses).
+constexpr int kMaxRowLabels = 256;
+
 // Response record of the segmented sum.
 struct RespItem {
   int32_t tok_begin;  // flat position of the response's first token

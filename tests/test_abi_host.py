@@ -141,6 +141,22 @@ def test_logprob_needs_a_prompt():
     assert binding.pp_workspace_size(wl.make_pack([0], [[5]]), 2, 1, 64)[0] > 0
 
 
+def test_logprob_bwd_argument_checks():
+    L = binding.lib()
+    fake = ctypes.c_void_p(16)
+    d, keep = _raw_desc([0, 5], [0], [1], [0], [5], 1)
+    assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 100, fake, fake, fake, fake, fake, 1 << 30, None) == 2
+    d, keep = _raw_desc([0, 12], [4], [2], [4, 7], [3, 3], 2)
+    assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 0, fake, fake, fake, fake, fake, 1 << 30, None) == 1
+    assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 100, fake, fake, None, fake, fake, 1 << 30, None) == 1
+    assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 100, fake, fake, fake, None, fake, 1 << 30, None) == 1
+    assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 100, fake, fake, fake, fake, fake, 1, None) == 4
+    # more responses per row than the backward stages per logit row
+    K = 257
+    d, keep = _raw_desc([0, 300], [10], [K], [10 + k for k in range(K)], [1] * K, K)
+    assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 100, fake, fake, fake, fake, fake, 1 << 30, None) == 3
+
+
 def test_loss_argument_checks():
     L = binding.lib()
     fake = ctypes.c_void_p(16)
