@@ -50,6 +50,12 @@ R11 Log-prob backward: the gradient reaching the logits is that of
     sum_{b,k} g_bk * seq_bk for given g = dL/dseq (the loss gradient); logit rows
     that predict no response token get 0, and a label outside the vocabulary
     makes its whole predicting row NaN (the forward makes the sum NaN).
+R12 Reward model: Sec. 2.1 only says the model maps a token sequence to a
+    scalar; we read it as a linear head on the hidden state of the sequence's
+    last token.  In the packed row the unpacked sequence (prompt, response k)
+    ends at o_k + L_k - 1, or at P - 1 when the response is empty (the prompt's
+    hidden states are those of the unpacked prompt, since a prompt token sees
+    only the prompt); a sequence with no token scores 0.
 
 All floating-point work is numpy float64.  Parity of every function here is
 pinned by tests against closed forms, brute force on tiny inputs, finite
@@ -352,6 +358,58 @@ def seq_logprob_grad(row_start, prompt_len, num_resp, resp_off, resp_len, logits
                 grad[src, y] += g
     grad[bad] = np.nan
     return grad
+
+
+def rm_score_rows(row_start, prompt_len, num_resp, resp_off, resp_len):
+    """Flat row whose hidden state scores each (row, response) slot (R12): the
+    last token of the unpacked sequence (prompt, response k), i.e. o_k + L_k - 1,
+    or the last prompt token P - 1 when the response is empty; -1 when the
+    sequence has no token at all or the slot is unused.  Returns [B, Kmax]."""
+    B = len(prompt_len)
+    Kmax = max([len(r) for r in resp_off] + [0])
+    out = np.full((B, Kmax), -1, dtype=np.int64)
+    for b in range(B):
+        r0, T, P, offs, lens = _row_fields(row_start, prompt_len, num_resp, resp_off, resp_len, b)
+        for kk, (o, L) in enumerate(zip(offs, lens)):
+            last = o + L - 1 if L > 0 else P - 1
+            out[b, kk] = r0 + last if last >= 0 else -1
+    return out
+
+
+def rm_scores(row_start, prompt_len, num_resp, resp_off, resp_len, hidden, w, bias=0.0):
+    """Reward-model scores (Sec. 2.1, R12): a linear head w . h + bias on the
+    hidden state that ends each (prompt, response) sequence.  hidden [sumT, H];
+    returns [B, Kmax] with 0 for unused slots and token-less sequences."""
+    hidden = np.asarray(hidden, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    rows = rm_score_rows(row_start, prompt_len, num_resp, resp_off, resp_len)
+    out = np.zeros(rows.shape)
+    for idx in np.ndindex(*rows.shape):
+        if rows[idx] >= 0:
+            out[idx] = float(hidden[rows[idx]] @ w) + bias
+    return out
+
+
+def rm_scores_grad(row_start, prompt_len, num_resp, resp_off, resp_len, hidden, w, dscores):
+    """Gradients of sum(dscores * rm_scores) with respect to hidden, w and bias:
+    dhidden[row] = sum of dscores over the slots read at that row, times w (0 on
+    every other row); dw = sum over slots of dscores * h_row; dbias = sum of the
+    dscores of the slots that have a row."""
+    hidden = np.asarray(hidden, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    dscores = np.asarray(dscores, dtype=np.float64)
+    rows = rm_score_rows(row_start, prompt_len, num_resp, resp_off, resp_len)
+    dh = np.zeros_like(hidden)
+    dw = np.zeros_like(w)
+    db = 0.0
+    for idx in np.ndindex(*rows.shape):
+        r = rows[idx]
+        if r >= 0:
+            g = float(dscores[idx])
+            dh[r] += g * w
+            dw += g * hidden[r]
+            db += g
+    return dh, dw, db
 
 
 def logprob_rows_needed(prompt_len, num_resp, resp_len):
