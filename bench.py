@@ -44,6 +44,7 @@ from paper_2602_24082_amd import workload as wl  # noqa: E402
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA (vendor, 2.4 GHz)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (vendor)
 LOGPROB_VOCAB = 128256      # Llama-3 vocabulary for the 8B-shaped workload
+HIDDEN_DIM = {32: 4096, 64: 8192}  # model width by query-head count (Llama-3-8B, Qwen2-72B)
 LOGPROB_SIGMA = 3.0
 DPO_BETA = 0.1
 
@@ -407,6 +408,30 @@ def main():
                        "traffic": traffic_from_profile("pp_logprob_bwd") if args.config == 1 else None}
     del dlogits
 
+    # reward-model head (scores on each response's last hidden state, then its
+    # backward) on the same pack, hidden size of the named model
+    hid = HIDDEN_DIM.get(cfg.hq, 4096)
+    hidden = wl.randn((T, hid), seed + 11, torch.bfloat16, dev)
+    w_head = wl.randn((hid,), seed + 12, torch.bfloat16, dev, sigma=0.02)
+    ws_rm = torch.empty(max(pp.pp_rm_workspace_size(pack), 1), dtype=torch.uint8, device=dev)
+    dsc = torch.ones(pack.num_rows, Kmax, device=dev)
+    for _ in range(2):
+        pp.pp_rm_scores(pack, hidden, w_head, 0.0, ws=ws_rm)
+        pp.pp_rm_scores_bwd(pack, hidden, w_head, dsc, ws=ws_rm)
+    torch.cuda.synchronize()
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    for _ in range(5):
+        pp.pp_rm_scores(pack, hidden, w_head, 0.0, ws=ws_rm)
+        pp.pp_rm_scores_bwd(pack, hidden, w_head, dsc, ws=ws_rm)
+    torch.cuda.synchronize()
+    pp.pp_timing_enable(False)
+    kr = pp.pp_timing_get()
+    rm_head = {"hidden_dim": hid, **{k: round(v[0] / v[1], 4) for k, v in kr.items() if k.startswith("pp_rm")},
+               "unit": "ms per launch",
+               "dhidden_GB_per_s": round(T * hid * 2 / (kr["pp_rm_dhidden"][0] / kr["pp_rm_dhidden"][1] * 1e-3) / 1e9, 1)}
+    del hidden
+
     comp = None
     if not args.no_comparator:
         padded = wl.unpacked_padded(pack)
@@ -446,6 +471,7 @@ def main():
         "comparator": comp,
         "logprob": logprob,
         "logprob_bwd": logprob_bwd,
+        "rm_head": rm_head,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,

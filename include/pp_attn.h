@@ -12,6 +12,8 @@
  *   pp_attn_bwd     its gradients dQ, dK, dV                   (Sec. 3.2)
  *   pp_seq_logprob  per-response summed token log-probs        (Sec. 2.1, Sec. 3.2)
  *   pp_seq_logprob_bwd  their gradient with respect to the logits
+ *   pp_rm_scores    reward-model head on each response's last token (Sec. 2.1)
+ *   pp_rm_scores_bwd    its gradients
  *   pp_dpo_loss     ranked-pair DPO / Bradley-Terry loss        (Sec. 2.1)
  *
  * Conventions shared by every entry point
@@ -161,6 +163,33 @@ pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vo
 pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
                              const void* logits, const int32_t* tokens, const float* dseq,
                              void* dlogits, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Reward-model head (Sec. 2.1: the reward model maps a token sequence to a
+ * scalar).  The score of the sequence (prompt b, response k) is
+ *   scores[b*K_max+k] = w . hidden[row] + bias,
+ * with row the last token of that unpacked sequence in the packed layout:
+ * row_start[b] + o_bk + L_bk - 1, or row_start[b] + P_b - 1 when the response
+ * is empty (a prompt token sees only the prompt, Sec. 3.2, so its hidden state
+ * is the unpacked one).  Slots k >= K_b and sequences without any token get 0.
+ * hidden (dev [sumT, hidden_dim], dtype), w (dev [hidden_dim], dtype), scores
+ * (dev float [B*K_max]); dot products accumulate in fp32.  The scores go to
+ * pp_dpo_loss with logp_ref = NULL for the Bradley-Terry loss.
+ * ws_bytes >= pp_rm_workspace_size's bytes. */
+pp_status pp_rm_workspace_size(const pp_pack_desc* desc, size_t* bytes);
+pp_status pp_rm_scores(const pp_pack_desc* desc, pp_dtype dtype, int hidden_dim, const void* hidden,
+                       const void* w, float bias, float* scores, void* ws, size_t ws_bytes,
+                       void* hip_stream);
+
+/* Backward of pp_rm_scores for dscores = dL/dscores (dev float [B*K_max]):
+ *   dhidden[row] = (sum of dscores over the slots scored at row) * w, and 0 on
+ *                  every other row (dev [sumT, hidden_dim], dtype, overwritten);
+ *   dw           = sum over scored slots of dscores * hidden[row] (dev float
+ *                  [hidden_dim], summed in slot order: deterministic);
+ *   *dbias       = sum of dscores over scored slots (dev float; may be NULL).
+ * Errors as pp_rm_scores. */
+pp_status pp_rm_scores_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hidden_dim, const void* hidden,
+                           const void* w, const float* dscores, void* dhidden, float* dw, float* dbias,
+                           void* ws, size_t ws_bytes, void* hip_stream);
 
 /* Ranked-pair DPO / Bradley-Terry loss (Sec. 2.1, extended to K > 2).
  * z_k = beta (logp_pol[b,k] - logp_ref[b,k]), or beta logp_pol[b,k] when

@@ -28,6 +28,7 @@ STATUS = {0: "PP_OK", 1: "PP_ERR_INVALID_ARGUMENT", 2: "PP_ERR_BAD_LAYOUT", 3: "
 
 EXPORTED = [
     "pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_seq_logprob_bwd", "pp_dpo_loss",
+    "pp_rm_workspace_size", "pp_rm_scores", "pp_rm_scores_bwd",
     "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
 ]
@@ -74,6 +75,9 @@ def lib() -> ctypes.CDLL:
     L.pp_attn_bwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, P, P, P, P, sz, P]
     L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_seq_logprob_bwd.argtypes = [D, i, i, P, P, P, P, P, sz, P]
+    L.pp_rm_workspace_size.argtypes = [D, ctypes.POINTER(sz)]
+    L.pp_rm_scores.argtypes = [D, i, i, P, P, ctypes.c_float, P, P, sz, P]
+    L.pp_rm_scores_bwd.argtypes = [D, i, i, P, P, P, P, P, P, P, sz, P]
     L.pp_dpo_loss.argtypes = [i32, i32, P, P, P, ctypes.c_float, P, P, P, P, sz, P]
     L.pp_pack_export.argtypes = [D, i, i, P, P, P, sz]
     L.pp_tile_class_len.argtypes = [D, i, i, ctypes.POINTER(sz)]
@@ -227,6 +231,46 @@ def pp_seq_logprob_bwd(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, d
     _check(lib().pp_seq_logprob_bwd(h.ref, _dtype_code(logits), V, _ptr(logits), _ptr(tokens), _ptr(dseq),
                                     _ptr(dlogits), _ptr(ws), ws.numel(), _stream(dev)))
     return dlogits
+
+
+def pp_rm_workspace_size(pack: Pack) -> int:
+    h = _DescHolder(pack)
+    n = ctypes.c_size_t(0)
+    _check(lib().pp_rm_workspace_size(h.ref, ctypes.byref(n)))
+    return n.value
+
+
+def pp_rm_scores(pack: Pack, hidden: torch.Tensor, w: torch.Tensor, bias: float = 0.0, scores=None, ws=None):
+    """Reward-model head scores [B, K_max] (float32) on each response's last token."""
+    H = hidden.shape[1]
+    if w.dtype != hidden.dtype or w.numel() != H:
+        raise TypeError("w must be [hidden_dim] in the dtype of hidden")
+    h = _DescHolder(pack)
+    dev = hidden.device
+    if scores is None:
+        scores = torch.empty(pack.num_rows, max(pack.max_resp, 1), dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = _workspace(pp_rm_workspace_size(pack), dev)
+    _check(lib().pp_rm_scores(h.ref, _dtype_code(hidden), H, _ptr(hidden), _ptr(w), float(bias), _ptr(scores),
+                              _ptr(ws), ws.numel(), _stream(dev)))
+    return scores
+
+
+def pp_rm_scores_bwd(pack: Pack, hidden: torch.Tensor, w: torch.Tensor, dscores: torch.Tensor, ws=None):
+    """(dhidden [sumT, H] in hidden's dtype, dw [H] float32, dbias [1] float32)."""
+    H = hidden.shape[1]
+    h = _DescHolder(pack)
+    dev = hidden.device
+    if dscores.dtype != torch.float32 or not dscores.is_contiguous():
+        raise TypeError("dscores must be contiguous float32 [B, K_max]")
+    dh = torch.empty_like(hidden)
+    dw = torch.empty(H, dtype=torch.float32, device=dev)
+    db = torch.empty(1, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = _workspace(pp_rm_workspace_size(pack), dev)
+    _check(lib().pp_rm_scores_bwd(h.ref, _dtype_code(hidden), H, _ptr(hidden), _ptr(w), _ptr(dscores), _ptr(dh),
+                                  _ptr(dw), _ptr(db), _ptr(ws), ws.numel(), _stream(dev)))
+    return dh, dw, db
 
 
 def pp_dpo_loss(num_resp, logp_pol: torch.Tensor, logp_ref: Optional[torch.Tensor], beta: float,

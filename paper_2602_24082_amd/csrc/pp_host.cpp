@@ -520,6 +520,56 @@ void plan_logprob(const Batch& bt, LogprobPlan* p) {
   p->r_tok = p->lay.add((size_t)bt.sumT * 4);
 }
 
+// Reward-model head: each (row, response) slot's hidden row, and the distinct
+// rows with the slots that read them.
+struct RmPlan {
+  std::vector<int64_t> slot_row;
+  std::vector<RmRowSlots> rows;
+  std::vector<int32_t> slots;
+  std::vector<int32_t> row_rec;
+  Layout lay;
+  size_t r_slot_row, r_rows, r_slots, r_row_rec;
+};
+
+void plan_rm(const Batch& bt, RmPlan* p) {
+  const int n = bt.B * bt.Kmax;
+  p->slot_row.assign(n, -1);
+  for (int b = 0; b < bt.B; ++b) {
+    const Row& r = bt.rows[b];
+    for (int k = 0; k < r.K; ++k) {
+      const int64_t last = r.len[k] > 0 ? (int64_t)r.off[k] + r.len[k] - 1 : (int64_t)r.P - 1;
+      if (last >= 0) p->slot_row[b * bt.Kmax + k] = r.tok0 + last;
+    }
+  }
+  p->row_rec.assign(bt.sumT, -1);
+  p->rows.clear();
+  p->slots.clear();
+  // distinct rows in order of first use, each with its slots in slot order
+  std::vector<std::vector<int32_t>> per_row;
+  for (int sidx = 0; sidx < n; ++sidx) {
+    const int64_t row = p->slot_row[sidx];
+    if (row < 0) continue;
+    int32_t& rec = p->row_rec[row];
+    if (rec < 0) {
+      rec = (int32_t)per_row.size();
+      per_row.emplace_back();
+      p->rows.push_back(RmRowSlots{row, 0, 0});
+    }
+    per_row[rec].push_back(sidx);
+  }
+  for (size_t i = 0; i < per_row.size(); ++i) {
+    p->rows[i].slot_off = (int32_t)p->slots.size();
+    p->rows[i].slot_cnt = (int32_t)per_row[i].size();
+    p->slots.insert(p->slots.end(), per_row[i].begin(), per_row[i].end());
+  }
+  p->lay = Layout();
+  p->r_slot_row = p->lay.add(p->slot_row.size() * 8);
+  p->r_rows = p->lay.add(p->rows.size() * sizeof(RmRowSlots));
+  p->r_slots = p->lay.add(p->slots.size() * 4);
+  p->r_row_rec = p->lay.add(p->row_rec.size() * 4);
+  p->lay.meta_bytes = p->lay.total;
+}
+
 pp_status check_logprob_layout(const Batch& bt) {
   for (int b = 0; b < bt.B; ++b) {
     const Row& r = bt.rows[b];
@@ -877,6 +927,91 @@ pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, in
   a.dtype = logits_dtype == PP_FP32 ? kFP32 : kBF16;
   hipError_t e = launch_logprob_bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "logprob backward launch");
+  return PP_OK;
+}
+
+pp_status pp_rm_workspace_size(const pp_pack_desc* desc, size_t* bytes) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if (!bytes) return fail(PP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  RmPlan p;
+  plan_rm(bt, &p);
+  *bytes = p.lay.total;
+  return PP_OK;
+}
+
+pp_status pp_rm_scores(const pp_pack_desc* desc, pp_dtype dtype, int hidden_dim, const void* hidden,
+                       const void* w, float bias, float* scores, void* ws, size_t ws_bytes,
+                       void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (hidden_dim < 1) return fail(PP_ERR_INVALID_ARGUMENT, "hidden_dim must be >= 1");
+  if (bt.Kmax == 0) return PP_OK;
+  if (!scores || !w || (bt.sumT > 0 && !hidden))
+    return fail(PP_ERR_INVALID_ARGUMENT, "hidden, w and scores must be non-NULL");
+  RmPlan p;
+  plan_rm(bt, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "rm head needs %zu workspace bytes, got %zu", p.lay.total, ws_bytes);
+  if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  hipStream_t s = (hipStream_t)hip_stream;
+  if ((st = stage_copy(ws, p.slot_row.data(), p.slot_row.size() * 8, s)) != PP_OK) return st;
+  RmLaunch a{};
+  a.hidden = hidden;
+  a.w = w;
+  a.bias = bias;
+  a.scores = scores;
+  a.slot_row = (const int64_t*)at(ws, p.lay, p.r_slot_row);
+  a.n_slots = (int)p.slot_row.size();
+  a.H = hidden_dim;
+  a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  hipError_t e = launch_rm_scores(a, s);
+  if (e != hipSuccess) return hip_fail(e, "rm scores launch");
+  return PP_OK;
+}
+
+pp_status pp_rm_scores_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hidden_dim, const void* hidden,
+                           const void* w, const float* dscores, void* dhidden, float* dw, float* dbias,
+                           void* ws, size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (hidden_dim < 1) return fail(PP_ERR_INVALID_ARGUMENT, "hidden_dim must be >= 1");
+  if (!w || !dw || (bt.sumT > 0 && (!hidden || !dhidden)) || (bt.Kmax > 0 && !dscores))
+    return fail(PP_ERR_INVALID_ARGUMENT, "hidden, w, dscores, dhidden and dw must be non-NULL");
+  RmPlan p;
+  plan_rm(bt, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "rm head needs %zu workspace bytes, got %zu", p.lay.total, ws_bytes);
+  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  hipStream_t s = (hipStream_t)hip_stream;
+  MetaImage img;
+  img.put(p.lay.regions[p.r_slot_row], p.slot_row.data(), p.slot_row.size() * 8);
+  img.put(p.lay.regions[p.r_rows], p.rows.data(), p.rows.size() * sizeof(RmRowSlots));
+  img.put(p.lay.regions[p.r_slots], p.slots.data(), p.slots.size() * 4);
+  img.put(p.lay.regions[p.r_row_rec], p.row_rec.data(), p.row_rec.size() * 4);
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  RmBwdLaunch a{};
+  a.hidden = hidden;
+  a.w = w;
+  a.dscores = dscores;
+  a.dhidden = dhidden;
+  a.dw = dw;
+  a.dbias = dbias;
+  a.slot_row = (const int64_t*)at(ws, p.lay, p.r_slot_row);
+  a.rows = (const RmRowSlots*)at(ws, p.lay, p.r_rows);
+  a.slots = (const int32_t*)at(ws, p.lay, p.r_slots);
+  a.row_rec = (const int32_t*)at(ws, p.lay, p.r_row_rec);
+  a.n_slots = (int)p.slot_row.size();
+  a.sumT = bt.sumT;
+  a.H = hidden_dim;
+  a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  hipError_t e = launch_rm_bwd(a, s);
+  if (e != hipSuccess) return hip_fail(e, "rm backward launch");
   return PP_OK;
 }
 

@@ -101,6 +101,36 @@ struct LogprobBwdLaunch {
 };
 hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s);
 
+struct RmLaunch {
+  const void* hidden;        // [sumT, H]
+  const void* w;             // [H]
+  float bias;
+  float* scores;             // [n_slots]
+  const int64_t* slot_row;   // [n_slots], -1 for slots without a row
+  int n_slots;
+  int H;
+  int dtype;
+};
+hipError_t launch_rm_scores(const RmLaunch& a, hipStream_t s);
+
+struct RmBwdLaunch {
+  const void* hidden;
+  const void* w;
+  const float* dscores;      // [n_slots]
+  void* dhidden;             // [sumT, H]
+  float* dw;                 // [H]
+  float* dbias;              // scalar or null
+  const int64_t* slot_row;
+  const RmRowSlots* rows;    // distinct rows read
+  const int32_t* slots;      // slot list of those rows
+  const int32_t* row_rec;    // [sumT]: record of each flat row or -1
+  int n_slots;
+  int sumT;
+  int H;
+  int dtype;
+};
+hipError_t launch_rm_bwd(const RmBwdLaunch& a, hipStream_t s);
+
 struct LossLaunch {
   const int32_t* num_resp;   // device copy [B]
   const float* pol;

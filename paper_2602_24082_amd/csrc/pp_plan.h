@@ -102,6 +102,15 @@ struct LogitRowItem {
   int32_t label_cnt;  // number of labels predicted from this row
 };
 
+// A hidden row read by the reward-model head and the slots (b * K_max + k)
+// that read it (an empty response reads the last prompt row, so several slots
+// can share one row).
+struct RmRowSlots {
+  int64_t row;       // flat hidden row
+  int32_t slot_off;  // first entry in the slot list
+  int32_t slot_cnt;
+};
+
 // Labels one logit row can predict in the log-prob backward (the last prompt
 // row predicts the first token of each of its K responses).
 constexpr int kMaxRowLabels = 256;

@@ -157,6 +157,23 @@ def test_logprob_bwd_argument_checks():
     assert L.pp_seq_logprob_bwd(ctypes.byref(d), 0, 100, fake, fake, fake, fake, fake, 1 << 30, None) == 3
 
 
+def test_rm_head_argument_checks():
+    L = binding.lib()
+    fake = ctypes.c_void_p(16)
+    d, keep = _raw_desc([0, 12], [4], [2], [4, 7], [3, 3], 2)
+    n = ctypes.c_size_t(0)
+    assert L.pp_rm_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0 and n.value > 0
+    assert L.pp_rm_workspace_size(ctypes.byref(d), None) == 1
+    assert L.pp_rm_scores(ctypes.byref(d), 0, 0, fake, fake, 0.0, fake, fake, 1 << 30, None) == 1
+    assert L.pp_rm_scores(ctypes.byref(d), 7, 64, fake, fake, 0.0, fake, fake, 1 << 30, None) == 1
+    assert L.pp_rm_scores(ctypes.byref(d), 0, 64, fake, None, 0.0, fake, fake, 1 << 30, None) == 1
+    assert L.pp_rm_scores(ctypes.byref(d), 0, 64, fake, fake, 0.0, fake, fake, 1, None) == 4
+    assert L.pp_rm_scores_bwd(ctypes.byref(d), 0, 64, fake, fake, None, fake, fake, None, fake, 1 << 30, None) == 1
+    assert L.pp_rm_scores_bwd(ctypes.byref(d), 0, 64, fake, fake, fake, fake, fake, None, fake, 1, None) == 4
+    bad, keep2 = _raw_desc([0, 12], [4], [2], [5, 7], [3, 3], 2)  # gap after the prompt
+    assert L.pp_rm_scores(ctypes.byref(bad), 0, 64, fake, fake, 0.0, fake, fake, 1 << 30, None) == 2
+
+
 def test_loss_argument_checks():
     L = binding.lib()
     fake = ctypes.c_void_p(16)
