@@ -141,6 +141,41 @@ def time_attention(pack, hq, hkv, d, dev, iters=10, warmup=3):
     return ms
 
 
+def comparator(pack, hq, hkv, d, dev):
+    """Attention fwd+bwd of the packed batch against the same samples unpacked
+    (prompt repeated per response: padded, and unpadded), and against a dense
+    causal kernel over the packed rows; plus the predicted ratios of the cost
+    model of Sec. 3.2.1 and the batch's KV bytes per layer."""
+    padded = wl.unpacked_padded(pack)
+    varlen = wl.unpacked_varlen(pack)
+    dense = wl.packed_dense_causal(pack)
+    t_packed = time_attention(pack, hq, hkv, d, dev)
+    t_pad = time_attention(padded, hq, hkv, d, dev)
+    t_var = time_attention(varlen, hq, hkv, d, dev)
+    t_dense = time_attention(dense, hq, hkv, d, dev)
+    comp = {"packed_ms": round(t_packed, 4), "unpacked_padded_ms": round(t_pad, 4),
+            "unpacked_varlen_ms": round(t_var, 4), "packed_dense_causal_ms": round(t_dense, 4),
+            "speedup_vs_padded": round(t_pad / t_packed, 3),
+            "speedup_vs_varlen": round(t_var / t_packed, 3),
+            "padded_layout": f"{padded.num_rows} sequences x {int(padded.row_lengths()[0])} tokens"}
+    st = pp.pp_pack_stats(pack)
+    kv = lambda tokens: int(tokens) * hkv * d * 2 * 2
+    cost = {
+        "eq1_cost_ratio": round(st["eq1_cost_ratio"], 4),
+        "eq1_predicted_speedup": round(1.0 / st["eq1_cost_ratio"], 3),
+        "rows_eq1_cheaper": f'{st["rows_eq1_cheaper"]}/{st["rows_with_responses"]}',
+        "measured_dense_packed_over_varlen": round(t_dense / t_var, 3),
+        "pairs_packed_over_unpacked": round(st["pairs_packed"] / st["pairs_unpacked"], 4),
+        "pairs_dense_packed_over_unpacked": round(st["pairs_dense_packed"] / st["pairs_unpacked"], 4),
+        "measured_packed_over_varlen": round(t_packed / t_var, 3),
+        "eq1_memory_ratio": round(st["eq1_memory_ratio"], 4),
+        "kv_bytes_per_layer": {"packed": kv(st["tokens_packed"]), "unpacked": kv(st["tokens_unpacked"]),
+                               "padded": kv(st["tokens_padded"])},
+        "kv_ratio_packed_over_unpacked": round(st["tokens_packed"] / st["tokens_unpacked"], 4),
+    }
+    return comp, cost
+
+
 def cpu_baseline(pack, cfg, rows, seed):
     """The oracle (fp64 numpy) on a bounded sample of the same workload: the
     attention forward and backward of the given rows, all heads."""
@@ -432,18 +467,12 @@ def main():
                "dhidden_GB_per_s": round(T * hid * 2 / (kr["pp_rm_dhidden"][0] / kr["pp_rm_dhidden"][1] * 1e-3) / 1e9, 1)}
     del hidden
 
-    comp = None
+    comp = cost = losing = None
     if not args.no_comparator:
-        padded = wl.unpacked_padded(pack)
-        varlen = wl.unpacked_varlen(pack)
-        t_packed = time_attention(pack, hq, cfg.hkv, d, dev)
-        t_pad = time_attention(padded, hq, cfg.hkv, d, dev)
-        t_var = time_attention(varlen, hq, cfg.hkv, d, dev)
-        comp = {"packed_ms": round(t_packed, 4), "unpacked_padded_ms": round(t_pad, 4),
-                "unpacked_varlen_ms": round(t_var, 4),
-                "speedup_vs_padded": round(t_pad / t_packed, 3),
-                "speedup_vs_varlen": round(t_var / t_packed, 3),
-                "padded_layout": f"{padded.num_rows} sequences x {int(padded.row_lengths()[0])} tokens"}
+        comp, cost = comparator(pack, hq, cfg.hkv, d, dev)
+        losing = comparator(wl.losing_regime_pack(), hq, cfg.hkv, d, dev)
+        losing = {"workload": "8 rows, prompt 32-96, K=2 responses 768-1024 (responses >> prompt)",
+                  **losing[0], **losing[1]}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -469,6 +498,8 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "speedup_vs_padded": comp["speedup_vs_padded"] if comp else None,
         "comparator": comp,
+        "cost_model": cost,
+        "losing_regime": losing,
         "logprob": logprob,
         "logprob_bwd": logprob_bwd,
         "rm_head": rm_head,

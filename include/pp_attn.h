@@ -219,6 +219,30 @@ pp_status pp_dpo_loss(int32_t num_rows, int32_t max_resp, const int32_t* num_res
 pp_status pp_pack_export(const pp_pack_desc* desc, int block_q, int block_k, int32_t* position_ids,
                          int32_t* segment_ids, uint8_t* tile_class, size_t tile_class_len);
 
+/* Cost and memory accounting of a packed batch against the unpacked layout
+ * that repeats each prompt once per response (host only, no GPU needed).
+ * "Unpacked" is the K_b sequences (prompt_b, response_bk) of every row;
+ * "padded" pads all of them to the longest one.  Rows with K_b = 0 count as
+ * their prompt alone on both sides. */
+typedef struct pp_pack_stats_t {
+  int64_t tokens_packed;      /* sum_b (P_b + sum_k L_bk)                          */
+  int64_t tokens_unpacked;    /* sum_b sum_k (P_b + L_bk)                          */
+  int64_t tokens_padded;      /* (number of unpacked sequences) x (longest one)    */
+  int64_t pairs_packed;       /* visible (query, key) pairs of the packed mask     */
+  int64_t pairs_unpacked;     /* causal pairs of the unpacked sequences            */
+  int64_t pairs_padded;       /* causal pairs of the padded sequences, padding incl. */
+  int64_t pairs_dense_packed; /* causal pairs of each packed row taken whole: the
+                                 work of a kernel that cannot skip the blocks that
+                                 hide one response from another                   */
+  double eq1_cost_ratio;      /* sum_b (P_b + sum_k L_bk)^2 / sum_b K_b (P_b + max_k L_bk)^2,
+                                 the cost model of Sec. 3.2.1 summed over rows     */
+  double eq1_memory_ratio;    /* the same with first powers (Sec. 3.2.1, linear-
+                                 memory attention)                                 */
+  int32_t rows_eq1_cheaper;   /* rows that satisfy Eq. (1)                          */
+  int32_t rows_with_responses;    /* rows with K_b >= 1                                 */
+} pp_pack_stats_t;
+pp_status pp_pack_stats(const pp_pack_desc* desc, pp_pack_stats_t* out);
+
 /* Number of tile_class entries pp_pack_export writes for (block_q, block_k). */
 pp_status pp_tile_class_len(const pp_pack_desc* desc, int block_q, int block_k, size_t* len);
 

@@ -28,10 +28,19 @@ STATUS = {0: "PP_OK", 1: "PP_ERR_INVALID_ARGUMENT", 2: "PP_ERR_BAD_LAYOUT", 3: "
 
 EXPORTED = [
     "pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_seq_logprob_bwd", "pp_dpo_loss",
-    "pp_rm_workspace_size", "pp_rm_scores", "pp_rm_scores_bwd",
+    "pp_rm_workspace_size", "pp_rm_scores", "pp_rm_scores_bwd", "pp_pack_stats",
     "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
 ]
+
+
+class PackStats(ctypes.Structure):
+    _fields_ = [("tokens_packed", ctypes.c_int64), ("tokens_unpacked", ctypes.c_int64),
+                ("tokens_padded", ctypes.c_int64), ("pairs_packed", ctypes.c_int64),
+                ("pairs_unpacked", ctypes.c_int64), ("pairs_padded", ctypes.c_int64),
+                ("pairs_dense_packed", ctypes.c_int64), ("eq1_cost_ratio", ctypes.c_double),
+                ("eq1_memory_ratio", ctypes.c_double), ("rows_eq1_cheaper", ctypes.c_int32),
+                ("rows_with_responses", ctypes.c_int32)]
 
 
 class PPError(RuntimeError):
@@ -76,6 +85,7 @@ def lib() -> ctypes.CDLL:
     L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_seq_logprob_bwd.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_rm_workspace_size.argtypes = [D, ctypes.POINTER(sz)]
+    L.pp_pack_stats.argtypes = [D, ctypes.POINTER(PackStats)]
     L.pp_rm_scores.argtypes = [D, i, i, P, P, ctypes.c_float, P, P, sz, P]
     L.pp_rm_scores_bwd.argtypes = [D, i, i, P, P, P, P, P, P, P, sz, P]
     L.pp_dpo_loss.argtypes = [i32, i32, P, P, P, ctypes.c_float, P, P, P, P, sz, P]
@@ -288,6 +298,14 @@ def pp_dpo_loss(num_resp, logp_pol: torch.Tensor, logp_ref: Optional[torch.Tenso
                              float(beta), _ptr(loss), _ptr(rows), _ptr(grad), _ptr(ws), ws.numel(),
                              _stream(dev)))
     return loss, rows, grad
+
+
+def pp_pack_stats(pack: Pack) -> dict:
+    """Host-only packed-versus-unpacked accounting (tokens, pairs, Eq. (1) ratios)."""
+    h = _DescHolder(pack)
+    out = PackStats()
+    _check(lib().pp_pack_stats(h.ref, ctypes.byref(out)))
+    return {name: getattr(out, name) for name, _ in PackStats._fields_}
 
 
 def pp_pack_export(pack: Pack, block_q: int = 128, block_k: int = 64, tiles: bool = True):

@@ -1054,6 +1054,54 @@ pp_status pp_dpo_loss(int32_t num_rows, int32_t max_resp, const int32_t* num_res
   return PP_OK;
 }
 
+pp_status pp_pack_stats(const pp_pack_desc* desc, pp_pack_stats_t* out) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if (!out) return fail(PP_ERR_INVALID_ARGUMENT, "out is NULL");
+  pp_pack_stats_t r{};
+  auto tri = [](int64_t n) { return n * (n + 1) / 2; };
+  double c_pp = 0, c_orig = 0, m_pp = 0, m_orig = 0;
+  int64_t n_seq = 0, longest = 0;
+  for (const Row& row : bt.rows) {
+    const int64_t P = row.P;
+    int64_t sum_l = 0, max_l = 0;
+    for (int k = 0; k < row.K; ++k) {
+      sum_l += row.len[k];
+      max_l = std::max<int64_t>(max_l, row.len[k]);
+    }
+    r.tokens_packed += P + sum_l;
+    r.pairs_packed += visible_pairs(row, 0, row.valid, 0, row.valid);
+    r.pairs_dense_packed += tri(P + sum_l);
+    if (row.K == 0) {
+      r.tokens_unpacked += P;
+      r.pairs_unpacked += tri(P);
+      ++n_seq;
+      longest = std::max(longest, P);
+      continue;
+    }
+    ++r.rows_with_responses;
+    for (int k = 0; k < row.K; ++k) {
+      r.tokens_unpacked += P + row.len[k];
+      r.pairs_unpacked += tri(P + row.len[k]);
+      ++n_seq;
+      longest = std::max<int64_t>(longest, P + row.len[k]);
+    }
+    const double a = (double)(P + sum_l), b = (double)(P + max_l);
+    c_pp += a * a;
+    c_orig += row.K * b * b;
+    m_pp += a;
+    m_orig += row.K * b;
+    if (a < std::sqrt((double)row.K) * b) ++r.rows_eq1_cheaper;
+  }
+  r.tokens_padded = n_seq * longest;
+  r.pairs_padded = n_seq * tri(longest);
+  r.eq1_cost_ratio = c_orig > 0 ? c_pp / c_orig : 0.0;
+  r.eq1_memory_ratio = m_orig > 0 ? m_pp / m_orig : 0.0;
+  *out = r;
+  return PP_OK;
+}
+
 pp_status pp_tile_class_len(const pp_pack_desc* desc, int block_q, int block_k, size_t* len) {
   Batch bt;
   pp_status st = read_desc(desc, &bt);

@@ -202,6 +202,26 @@ def unpacked_varlen(pack: Pack) -> Pack:
     return make_pack(seqs, [[] for _ in seqs], max_resp=0)
 
 
+def packed_dense_causal(pack: Pack) -> Pack:
+    """Cost comparator for a kernel that cannot skip the blocks hiding one
+    response from another: each packed row's real tokens attended causally as one
+    sequence (a prompt-only row of P_b + sum_k L_bk tokens).  Its outputs are not
+    the packed semantics; only its work matters (the dense cost of Sec. 3.2.1)."""
+    lens = [int(pack.prompt_len[b]) + int(pack.resp_len[b, :int(pack.num_resp[b])].sum())
+            for b in range(pack.num_rows)]
+    return make_pack(lens, [[] for _ in lens], max_resp=0)
+
+
+def losing_regime_pack(rows: int = 8, seed: int = 231) -> Pack:
+    """Responses much longer than the prompt (prompt uniform 32-96, K = 2
+    responses uniform 768-1024): the regime where Eq. (1) predicts that packing
+    costs more than the unpacked layout for dense attention."""
+    rng = np.random.default_rng(np.random.SeedSequence([2602, 24082, seed]))
+    P = [int(x) for x in rng.integers(32, 97, size=rows)]
+    L = [[int(x) for x in rng.integers(768, 1025, size=2)] for _ in range(rows)]
+    return make_pack(P, L)
+
+
 # ----------------------------------------------------------------------------
 # Random tensors
 # ----------------------------------------------------------------------------

@@ -174,6 +174,42 @@ def test_rm_head_argument_checks():
     assert L.pp_rm_scores(ctypes.byref(bad), 0, 64, fake, fake, 0.0, fake, fake, 1 << 30, None) == 2
 
 
+def test_pack_stats_against_oracle():
+    # single rows: the ratios are the oracle's per-data-point cost model (pinned
+    # against Table 1); multi-row batches: counts against explicit masks
+    for P, lens in [(228, [251, 130]), (720, [469, 331]), (600, [110, 90]), (64, [1000, 900]), (5, [0, 3, 7])]:
+        st = binding.pp_pack_stats(wl.make_pack([P], [lens]))
+        nz = [L for L in lens]
+        assert st["eq1_cost_ratio"] == pytest.approx(orc.cost_ratio(P, nz), rel=1e-12)
+        assert st["eq1_memory_ratio"] == pytest.approx(orc.memory_ratio(P, nz), rel=1e-12)
+        assert st["rows_eq1_cheaper"] == int(orc.packing_is_cheaper(P, nz))
+    rng = np.random.default_rng(11)
+    for _ in range(6):
+        pack = _random_pack(rng, zero_prompt_ok=True)
+        st = binding.pp_pack_stats(pack)
+        args = pack.oracle_args()
+        packed = unpacked = dense = tok_p = tok_u = 0
+        seqs = []
+        for b in range(pack.num_rows):
+            r0, T, P, offs, lens = orc._row_fields(*args, b)
+            packed += int(orc.row_mask(T, P, offs, lens).sum())
+            n = P + sum(lens)
+            dense += n * (n + 1) // 2
+            tok_p += n
+            for L in (lens if lens else [0]):
+                m = orc.row_mask(P + L, P, [P], [L]) if lens else orc.row_mask(P, P, [], [])
+                unpacked += int(m.sum())
+                tok_u += P + L
+                seqs.append(P + L)
+        assert st["pairs_packed"] == packed == orc.useful_pairs(pack.prompt_len, pack.num_resp, pack.resp_len)
+        assert st["pairs_unpacked"] == unpacked and st["pairs_dense_packed"] == dense
+        assert st["tokens_packed"] == tok_p and st["tokens_unpacked"] == tok_u
+        assert st["tokens_padded"] == len(seqs) * max(seqs)
+        assert st["rows_eq1_cheaper"] == sum(
+            int(orc.packing_is_cheaper(int(pack.prompt_len[b]), list(pack.resp_len[b, :int(pack.num_resp[b])])))
+            for b in range(pack.num_rows) if int(pack.num_resp[b]) > 0)
+
+
 def test_loss_argument_checks():
     L = binding.lib()
     fake = ctypes.c_void_p(16)
