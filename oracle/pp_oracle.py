@@ -46,11 +46,11 @@ R9  Softmax scale 1/sqrt(d) unless given; q-head h uses kv-head floor(h/G).
 R10 Padding tokens: attention output, LSE and all gradients are 0; an empty
     response scores 0; rows with fewer than two responses are left out of the
     loss mean.
-R11 Log-prob backward: the gradient reaching the logits is that of
+R16 Log-prob backward: the gradient reaching the logits is that of
     sum_{b,k} g_bk * seq_bk for given g = dL/dseq (the loss gradient); logit rows
     that predict no response token get 0, and a label outside the vocabulary
     makes its whole predicting row NaN (the forward makes the sum NaN).
-R12 Reward model: Sec. 2.1 only says the model maps a token sequence to a
+R17 Reward model: Sec. 2.1 only says the model maps a token sequence to a
     scalar; we read it as a linear head on the hidden state of the sequence's
     last token.  In the packed row the unpacked sequence (prompt, response k)
     ends at o_k + L_k - 1, or at P - 1 when the response is empty (the prompt's
@@ -327,7 +327,7 @@ def seq_logprob(row_start, prompt_len, num_resp, resp_off, resp_len, logits, tok
 
 
 def seq_logprob_grad(row_start, prompt_len, num_resp, resp_off, resp_len, logits, tokens, dseq):
-    """Gradient of sum_{b,k} dseq[b,k] * seq[b,k] with respect to the logits (R11).
+    """Gradient of sum_{b,k} dseq[b,k] * seq[b,k] with respect to the logits (R16).
 
     seq is seq_logprob's per-response sum, so every response token contributes
     dseq[b,k] * (onehot(label) - softmax(predicting row)) to the row that
@@ -361,7 +361,7 @@ def seq_logprob_grad(row_start, prompt_len, num_resp, resp_off, resp_len, logits
 
 
 def rm_score_rows(row_start, prompt_len, num_resp, resp_off, resp_len):
-    """Flat row whose hidden state scores each (row, response) slot (R12): the
+    """Flat row whose hidden state scores each (row, response) slot (R17): the
     last token of the unpacked sequence (prompt, response k), i.e. o_k + L_k - 1,
     or the last prompt token P - 1 when the response is empty; -1 when the
     sequence has no token at all or the slot is unused.  Returns [B, Kmax]."""
@@ -377,7 +377,7 @@ def rm_score_rows(row_start, prompt_len, num_resp, resp_off, resp_len):
 
 
 def rm_scores(row_start, prompt_len, num_resp, resp_off, resp_len, hidden, w, bias=0.0):
-    """Reward-model scores (Sec. 2.1, R12): a linear head w . h + bias on the
+    """Reward-model scores (Sec. 2.1, R17): a linear head w . h + bias on the
     hidden state that ends each (prompt, response) sequence.  hidden [sumT, H];
     returns [B, Kmax] with 0 for unused slots and token-less sequences."""
     hidden = np.asarray(hidden, dtype=np.float64)

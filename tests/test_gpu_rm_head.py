@@ -1,5 +1,5 @@
 """GPU parity of the reward-model head (pp_rm_scores / pp_rm_scores_bwd) against
-the fp64 oracle (reading R12).
+the fp64 oracle (reading R17).
 
 Tolerances from the arithmetic: a score is an fp32 dot product of H products
 of exact inputs, so its error is bounded by ~H * 2^-24 * sum|h_i w_i| (held to

@@ -1,4 +1,4 @@
-"""Pins of the oracle's log-prob backward (reading R11) against facts that do
+"""Pins of the oracle's log-prob backward (reading R16) against facts that do
 not come from the oracle's own formula: central finite differences of the
 (separately pinned) forward, the softmax simplex, the sharing of the last prompt
 row by every response (Sec. 3.2), and the rows that predict nothing."""

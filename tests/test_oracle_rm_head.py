@@ -1,4 +1,4 @@
-"""Pins of the oracle's reward-model head (reading R12): packing gives the score
+"""Pins of the oracle's reward-model head (reading R17): packing gives the score
 of each unpacked (prompt, response) sequence (Sec. 3.2), the head is linear
 (closed forms), its gradients match central finite differences, and the scores
 feed the Bradley-Terry loss of Sec. 2.1 unchanged."""
