@@ -100,14 +100,25 @@ typedef __attribute__((address_space(3))) void lds_void;
 // address `lds_dst` (wave-uniform, passed through M0) + 16*l.  Every kernel
 // waits for these explicitly (wait_vmem / wait_tile) before the barrier that
 // publishes a stage, and reads a stage only after that barrier.
+//
+// The instruction is issued as inline assembly rather than through the
+// compiler builtin.  The compiler cannot tell which LDS bytes an LDS DMA
+// writes, so after the builtin it waits for every outstanding DMA before the
+// next LDS read it cannot prove disjoint (in practice the first transposed
+// read of each tile) -- which includes the prefetch of the NEXT tile and so
+// serialises the prefetch with half of the compute it should overlap.  The
+// kernels' own waits are exact; the "memory" clobber keeps the compiler from
+// moving LDS accesses across the statement, and M0 is set inside it.
 __device__ __forceinline__ void lds_dma16(const void* src, const void* lds_dst) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds_dst, 16, 0, 0);
+  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_void*)lds_dst);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(base) : "memory", "m0");
 }
 
 // One 4-byte element per lane into LDS (lane l -> lds + 4*l): the per-query
-// scalars of a 64-query tile.
+// scalars of a 64-query tile.  Issued like lds_dma16.
 __device__ __forceinline__ void dma_dword(void* lds, const void* src) {
-  __builtin_amdgcn_global_load_lds(src, (lds_void*)lds, 4, 0, 0);
+  const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_void*)lds);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(base) : "memory", "m0");
 }
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
@@ -237,8 +248,17 @@ constexpr int kSchedDsRead = 0x100;
 // (so a branch on it does not make a loop divergent).
 __device__ __forceinline__ bool wave_any(bool x) { return __builtin_amdgcn_readfirstlane(__any(x)) != 0; }
 
-// A plan record read so that the compiler keeps every field in scalar
-// registers (the record is the same for the whole workgroup).
+// A read-only plan record at a wave-uniform address, fetched with scalar loads
+// (through the constant address space) so that it lands in scalar registers
+// and is waited for on the scalar counter.  A vector load would be followed by
+// a wait on the vector-memory counter, which also waits for every LDS DMA
+// issued before it, including prefetches meant to stay in flight.
+// Each 32-bit field is loaded on its own: an aggregate copy is lowered to
+// loads the backend keeps on the vector path.
+__device__ __forceinline__ int32_t scalar_load(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
 template <typename Item>
 __device__ __forceinline__ Item load_uniform(const Item* p) {
   static_assert(sizeof(Item) % 4 == 0, "plan records are made of 32-bit fields");
@@ -246,15 +266,8 @@ __device__ __forceinline__ Item load_uniform(const Item* p) {
   const int32_t* src = reinterpret_cast<const int32_t*>(p);
   int32_t* dst = reinterpret_cast<int32_t*>(&out);
 #pragma unroll
-  for (int i = 0; i < (int)(sizeof(Item) / 4); ++i) dst[i] = __builtin_amdgcn_readfirstlane(src[i]);
+  for (int i = 0; i < (int)(sizeof(Item) / 4); ++i) dst[i] = scalar_load(src + i);
   return out;
-}
-
-// A read-only 32-bit value at a wave-uniform address, fetched with a scalar
-// load (through the constant address space) instead of a vector load whose
-// latency the wave would otherwise wait out in full.
-__device__ __forceinline__ int32_t scalar_load(const int32_t* p) {
-  return *(const __attribute__((address_space(4))) int32_t*)p;
 }
 
 // Maps a linear workgroup index to (item, head).  Workgroups are dispatched to
