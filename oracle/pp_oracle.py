@@ -56,6 +56,13 @@ R17 Reward model: Sec. 2.1 only says the model maps a token sequence to a
     ends at o_k + L_k - 1, or at P - 1 when the response is empty (the prompt's
     hidden states are those of the unpacked prompt, since a prompt token sees
     only the prompt); a sequence with no token scores 0.
+R19 Rotary position embedding: the paper states only that packed tokens keep
+    their original position IDs (Sec. 3.2); the models it trains (Llama, Qwen)
+    encode those IDs with rotary embeddings.  We use the half-split form of
+    those models: for j < d/2, frequency w_j = base^(-2j/d), and the pair
+    (x_j, x_{j+d/2}) of a token at position p is rotated by the angle p * w_j
+    (counter-clockwise: x_j cos - x_{j+d/2} sin, x_{j+d/2} cos + x_j sin),
+    applied to queries and keys before the attention scores.
 
 All floating-point work is numpy float64.  Parity of every function here is
 pinned by tests against closed forms, brute force on tiny inputs, finite
@@ -276,6 +283,64 @@ def attn_bwd(row_start, prompt_len, num_resp, resp_off, resp_len, q, k, v, dout,
             dq[r0:r0 + T, h, :] = scale * (dS @ Kg)
             dk[r0:r0 + T, g, :] += scale * (dS.T @ Qh)
     return dq, dk, dv
+
+
+# ----------------------------------------------------------------------------
+# Rotary position embedding with the packed position IDs (Sec. 3.2, R2, R19)
+# ----------------------------------------------------------------------------
+
+
+def rope_angles(pos, d: int, base: float) -> np.ndarray:
+    """Rotation angle of every (token, pair) [n, d/2]: pos * base^(-2j/d) (R19)."""
+    pos = np.asarray(pos, dtype=np.float64)
+    j = np.arange(d // 2, dtype=np.float64)
+    w = base ** (-2.0 * j / d)
+    return pos[:, None] * w[None, :]
+
+
+def rope(x, pos, base: float, inverse: bool = False) -> np.ndarray:
+    """Rotate every head of every token by its position (R19).
+
+    x: [n, H, d]; pos: [n].  Pair j is (x[..., j], x[..., j + d/2]).  With
+    inverse=True the rotation is undone (the transpose of the rotation, which is
+    also the map that carries a gradient back through it).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    d = x.shape[2]
+    a = rope_angles(pos, d, base)[:, None, :]          # [n, 1, d/2]
+    c, s = np.cos(a), np.sin(a)
+    if inverse:
+        s = -s
+    x1, x2 = x[..., : d // 2], x[..., d // 2:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def pack_rope(row_start, prompt_len, num_resp, resp_off, resp_len, x, base, inverse=False):
+    """RoPE over the flat token axis with the packed position IDs (R2)."""
+    pos = pack_position_ids(row_start, prompt_len, num_resp, resp_off, resp_len)
+    return rope(x, pos, base, inverse)
+
+
+def attn_fwd_rope(row_start, prompt_len, num_resp, resp_off, resp_len, q, k, v, base, scale=None):
+    """Attention of rotated queries and keys: returns O, LSE and the rotated q, k."""
+    args = (row_start, prompt_len, num_resp, resp_off, resp_len)
+    qr = pack_rope(*args, q, base)
+    kr = pack_rope(*args, k, base)
+    O, LSE = attn_fwd(*args, qr, kr, v, scale)
+    return O, LSE, qr, kr
+
+
+def attn_bwd_rope(row_start, prompt_len, num_resp, resp_off, resp_len, q, k, v, dout, base, scale=None):
+    """Gradients of sum(dout * O) with respect to the UN-rotated q and k, and v.
+
+    The attention gradients with respect to the rotated q and k are carried back
+    through the rotation by its transpose (the inverse rotation).
+    """
+    args = (row_start, prompt_len, num_resp, resp_off, resp_len)
+    qr = pack_rope(*args, q, base)
+    kr = pack_rope(*args, k, base)
+    dqr, dkr, dv = attn_bwd(*args, qr, kr, v, dout, scale)
+    return pack_rope(*args, dqr, base, inverse=True), pack_rope(*args, dkr, base, inverse=True), dv
 
 
 # ----------------------------------------------------------------------------
