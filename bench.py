@@ -46,6 +46,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (vendor)
 LOGPROB_VOCAB = 128256      # Llama-3 vocabulary for the 8B-shaped workload
 HIDDEN_DIM = {32: 4096, 64: 8192}  # model width by query-head count (Llama-3-8B, Qwen2-72B)
 LOGPROB_SIGMA = 3.0
+ROPE_BASE = {32: 500000.0, 64: 1000000.0}  # rotary base by query-head count (Llama-3, Qwen2)
 DPO_BETA = 0.1
 
 
@@ -288,6 +289,62 @@ def chain_sorting(dev, reps=1):
                       "config": {"workload": cfg.name, "vocab": V, "beta": cfg.beta}, "cells": cells}))
 
 
+def rope_leg(pack, cfg, seed, dev, base, iters=10):
+    """Attention fwd+bwd with rotary embeddings on the packed position IDs: the
+    fused entry points (queries rotated in the forward's prologue, dq and dk
+    rotated back in the backward's epilogues, keys rotated once) against the
+    same work done as separate passes (pp_rope on q and k, plain attention,
+    pp_rope inverse on dq and dk), and plain attention without rotation."""
+    hq, hkv, d = cfg.hq, cfg.hkv, cfg.head_dim
+    a = Attn(pack, hq, hkv, d, seed, dev)
+    q_rot, k_rot = torch.empty_like(a.q), torch.empty_like(a.k)
+    ws_r = torch.empty(pp.pp_rope_workspace_size(pack, d), dtype=torch.uint8, device=dev)
+
+    def fused():
+        pp.pp_attn_fwd_rope(pack, a.q, a.k, a.v, base, out=a.o, lse=a.lse, q_rot=q_rot, k_rot=k_rot, ws=a.ws_f)
+        pp.pp_attn_bwd_rope(pack, q_rot, k_rot, a.v, a.o, a.lse, a.do, base, dq=a.dq, dk=a.dk, dv=a.dv, ws=a.ws_b)
+
+    def separate():
+        pp.pp_rope(pack, a.q, base, out=q_rot, ws=ws_r)
+        pp.pp_rope(pack, a.k, base, out=k_rot, ws=ws_r)
+        pp.pp_attn_fwd(pack, q_rot, k_rot, a.v, out=a.o, lse=a.lse, ws=a.ws_f)
+        pp.pp_attn_bwd(pack, q_rot, k_rot, a.v, a.o, a.lse, a.do, dq=a.dq, dk=a.dk, dv=a.dv, ws=a.ws_b)
+        pp.pp_rope(pack, a.dq, base, inverse=True, out=a.dq, ws=ws_r)
+        pp.pp_rope(pack, a.dk, base, inverse=True, out=a.dk, ws=ws_r)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(iters):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / iters
+
+    t_plain = timed(a.run)
+    t_fused = timed(fused)
+    t_sep = timed(separate)
+    # the standalone rotation of q alone: bytes = read + write of q (bf16)
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    timed(lambda: pp.pp_rope(pack, a.q, base, out=q_rot, ws=ws_r))
+    pp.pp_timing_enable(False)
+    kr = pp.pp_timing_get()["pp_rope"]
+    q_bytes = pack.total_tokens * hq * d * 2 * 2
+    gbs = q_bytes / (kr[0] / kr[1] * 1e-3) / 1e9
+    out = {"rope_base": base, "fused_fwd_bwd_ms": round(t_fused, 4), "separate_passes_ms": round(t_sep, 4),
+           "plain_attention_ms": round(t_plain, 4), "fused_over_plain": round(t_fused / t_plain, 3),
+           "separate_over_fused": round(t_sep / t_fused, 3),
+           "pp_rope_q": {"avg_ms": round(kr[0] / kr[1], 4), "GB_per_s": round(gbs, 1),
+                         "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": q_bytes}}
+    del a
+    torch.cuda.empty_cache()
+    return out
+
+
 def calib_copy(dev):
     """A plain device copy of 1 GiB, five times: read 1 GiB + write 1 GiB each."""
     n = 1 << 30
@@ -409,6 +466,14 @@ def main():
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": work, "avg_launch_ms": round(avg_ms, 4)}
     kernels = {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in kern.items()}
+    # every attention kernel against the bf16 MFMA peak (algorithmic FLOPs per launch)
+    attn_roofs = {}
+    for k in ("pp_attn_fwd", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq"):
+        if k in kern:
+            k_ms = kern[k][0] / kern[k][1]
+            ach = per_launch[k][1] / (k_ms * 1e-3) / 1e12
+            attn_roofs[k] = {"achieved_TFLOP_s": round(ach, 1), "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                             "avg_ms": round(k_ms, 4), "algorithmic_flops_per_launch": per_launch[k][1]}
     lp = kern.get("pp_logprob_rows")
     logprob = None
     if lp:
@@ -467,6 +532,8 @@ def main():
                "dhidden_GB_per_s": round(T * hid * 2 / (kr["pp_rm_dhidden"][0] / kr["pp_rm_dhidden"][1] * 1e-3) / 1e9, 1)}
     del hidden
 
+    rope = rope_leg(pack, cfg, seed, dev, ROPE_BASE.get(cfg.hq, 500000.0))
+
     comp = cost = losing = None
     if not args.no_comparator:
         comp, cost = comparator(pack, hq, cfg.hkv, d, dev)
@@ -503,7 +570,9 @@ def main():
         "logprob": logprob,
         "logprob_bwd": logprob_bwd,
         "rm_head": rm_head,
+        "rope": rope,
         "kernels": kernels,
+        "attention_rooflines": attn_roofs,
         "roofline": roof,
         "cpu_baseline": cpu,
         "loss": loss_val,

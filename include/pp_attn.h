@@ -15,6 +15,9 @@
  *   pp_rm_scores    reward-model head on each response's last token (Sec. 2.1)
  *   pp_rm_scores_bwd    its gradients
  *   pp_dpo_loss     ranked-pair DPO / Bradley-Terry loss        (Sec. 2.1)
+ *   pp_rope, pp_attn_fwd_rope, pp_attn_bwd_rope
+ *                   rotary position embedding on the packed position IDs
+ *                   (Sec. 3.2), alone or fused into attention
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -130,6 +133,50 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
                       float scale, const void* q, const void* k, const void* v, const void* o,
                       const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
                       size_t ws_bytes, void* hip_stream);
+
+/* Rotary position embedding on the packed position IDs.  Sec. 3.2 requires that
+ * every packed token keep the position it has in its unpacked sequence: prompt
+ * token t has position t, token j of a response has P_b + j (so every response
+ * continues from the end of the shared prompt), padding has 0 -- the
+ * position_ids of pp_pack_export.  The embedding is the half-split rotary form
+ * of the Llama / Qwen models: for j < head_dim/2 the pair (x_j, x_{j+head_dim/2})
+ * of a token at position p is rotated by the angle p * rope_base^(-2j/head_dim),
+ *   y_j = x_j cos - x_{j+d/2} sin,   y_{j+d/2} = x_{j+d/2} cos + x_j sin.
+ * inverse != 0 applies the transpose (the rotation by the negative angle), which
+ * is also the map that carries a gradient back through the embedding.  Angles
+ * are formed and reduced to [-pi, pi] in fp64, sines and cosines and the
+ * rotation are fp32, bf16 outputs are rounded to nearest even.
+ * x, y: dev [sumT, heads, head_dim] in dtype; y may equal x (in place).
+ * head_dim a multiple of 8 in [8, 1024] (PP_ERR_UNSUPPORTED otherwise);
+ * rope_base finite and > 0 (PP_ERR_INVALID_ARGUMENT otherwise).
+ * ws_bytes >= pp_rope_workspace_size's bytes (positions and frequencies). */
+pp_status pp_rope_workspace_size(const pp_pack_desc* desc, int head_dim, size_t* bytes);
+pp_status pp_rope(const pp_pack_desc* desc, pp_dtype dtype, int heads, int head_dim, float rope_base,
+                  int inverse, const void* x, void* y, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* pp_attn_fwd of rotated queries and keys (the rotation of pp_rope): q and k are
+ * the un-rotated inputs.  k is rotated once into k_rot (dev [sumT, hkv,
+ * head_dim], dtype, required); each query row is rotated in registers inside the
+ * attention kernel right after it is loaded, and written to q_rot (dev [sumT,
+ * hq, head_dim], dtype) when q_rot is not NULL.  For PP_FP32 the queries are
+ * rounded to bf16 before they are rotated, as for attention.  o and lse are those
+ * of pp_attn_fwd(rope(q), rope(k), v).  Workspace: pp_workspace_size's fwd.
+ * Errors as pp_attn_fwd, plus PP_ERR_INVALID_ARGUMENT for a bad rope_base or a
+ * NULL k_rot. */
+pp_status pp_attn_fwd_rope(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                           float scale, float rope_base, const void* q, const void* k, const void* v,
+                           void* o, float* lse, void* q_rot, void* k_rot, void* ws, size_t ws_bytes,
+                           void* hip_stream);
+
+/* Backward of pp_attn_fwd_rope: takes the rotated q_rot and k_rot (as written by
+ * pp_attn_fwd_rope), v, o, lse and dout, and writes dq and dk with respect to
+ * the UN-rotated q and k -- the dQ and dK/dV kernels rotate their gradient rows
+ * back (the inverse rotation) just before storing them -- and dv.  Otherwise as
+ * pp_attn_bwd (deterministic; workspace pp_workspace_size's bwd). */
+pp_status pp_attn_bwd_rope(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                           float scale, float rope_base, const void* q_rot, const void* k_rot,
+                           const void* v, const void* o, const float* lse, const void* dout, void* dq,
+                           void* dk, void* dv, void* ws, size_t ws_bytes, void* hip_stream);
 
 /* Per-response sequence log-probabilities (Sec. 2.1 scores, Sec. 3.2 layout).
  * Token j of response k of row b sits at row-relative position t = o_bk + j; it

@@ -31,6 +31,7 @@ EXPORTED = [
     "pp_rm_workspace_size", "pp_rm_scores", "pp_rm_scores_bwd", "pp_pack_stats",
     "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
+    "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
 ]
 
 
@@ -82,6 +83,11 @@ def lib() -> ctypes.CDLL:
                                     ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.pp_attn_fwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, sz, P]
     L.pp_attn_bwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, P, P, P, P, sz, P]
+    f32 = ctypes.c_float
+    L.pp_rope_workspace_size.argtypes = [D, i, ctypes.POINTER(sz)]
+    L.pp_rope.argtypes = [D, i, i, i, f32, i, P, P, P, sz, P]
+    L.pp_attn_fwd_rope.argtypes = [D, i, i, i, i, f32, f32, P, P, P, P, P, P, P, P, sz, P]
+    L.pp_attn_bwd_rope.argtypes = [D, i, i, i, i, f32, f32, P, P, P, P, P, P, P, P, P, P, sz, P]
     L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_seq_logprob_bwd.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_rm_workspace_size.argtypes = [D, ctypes.POINTER(sz)]
@@ -200,6 +206,65 @@ def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, 
     _check(lib().pp_attn_bwd(h.ref, _dtype_code(q), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v),
                              _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),
                              ws.numel(), _stream(q.device)))
+    return dq, dk, dv
+
+
+def pp_rope_workspace_size(pack: Pack, head_dim: int) -> int:
+    h = _DescHolder(pack)
+    n = ctypes.c_size_t(0)
+    _check(lib().pp_rope_workspace_size(h.ref, head_dim, ctypes.byref(n)))
+    return n.value
+
+
+def pp_rope(pack: Pack, x: torch.Tensor, rope_base: float, inverse: bool = False, out=None, ws=None):
+    """Rotary embedding of x [sumT, heads, d] on the packed position IDs; out may be x."""
+    T, H, d = x.shape
+    h = _DescHolder(pack)
+    out = torch.empty_like(x) if out is None else out
+    if ws is None:
+        ws = _workspace(pp_rope_workspace_size(pack, d), x.device)
+    _check(lib().pp_rope(h.ref, _dtype_code(x), H, d, float(rope_base), int(bool(inverse)), _ptr(x), _ptr(out),
+                         _ptr(ws), ws.numel(), _stream(x.device)))
+    return out
+
+
+def pp_attn_fwd_rope(pack: Pack, q, k, v, rope_base: float, scale: float = 0.0, want_q_rot: bool = True,
+                     out=None, lse=None, q_rot=None, k_rot=None, ws=None):
+    """Attention of rotated q, k (rotation fused into the forward); returns
+    (o, lse, q_rot or None, k_rot)."""
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    h = _DescHolder(pack)
+    out = torch.empty_like(q) if out is None else out
+    if lse is None:
+        lse = torch.empty(hq, T, dtype=torch.float32, device=q.device)
+    if want_q_rot and q_rot is None:
+        q_rot = torch.empty_like(q)
+    k_rot = torch.empty_like(k) if k_rot is None else k_rot
+    if ws is None:
+        nb = pp_workspace_size(pack, hq, hkv, d, fwd=True, bwd=False, loss=False, dtype=_dtype_code(q))[0]
+        ws = _workspace(nb, q.device)
+    _check(lib().pp_attn_fwd_rope(h.ref, _dtype_code(q), hq, hkv, d, float(scale), float(rope_base), _ptr(q),
+                                  _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(q_rot), _ptr(k_rot), _ptr(ws),
+                                  ws.numel(), _stream(q.device)))
+    return out, lse, q_rot, k_rot
+
+
+def pp_attn_bwd_rope(pack: Pack, q_rot, k_rot, v, o, lse, dout, rope_base: float, scale: float = 0.0,
+                     dq=None, dk=None, dv=None, ws=None):
+    """Backward of pp_attn_fwd_rope: (dq, dk) with respect to the un-rotated q, k, and dv."""
+    T, hq, d = q_rot.shape
+    hkv = k_rot.shape[1]
+    h = _DescHolder(pack)
+    dq = torch.empty_like(q_rot) if dq is None else dq
+    dk = torch.empty_like(k_rot) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    if ws is None:
+        nb = pp_workspace_size(pack, hq, hkv, d, fwd=False, bwd=True, loss=False, dtype=_dtype_code(q_rot))[1]
+        ws = _workspace(nb, q_rot.device)
+    _check(lib().pp_attn_bwd_rope(h.ref, _dtype_code(q_rot), hq, hkv, d, float(scale), float(rope_base),
+                                  _ptr(q_rot), _ptr(k_rot), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq),
+                                  _ptr(dk), _ptr(dv), _ptr(ws), ws.numel(), _stream(q_rot.device)))
     return dq, dk, dv
 
 

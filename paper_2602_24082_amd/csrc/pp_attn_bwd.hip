@@ -24,6 +24,11 @@
 // All products run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Q, K, V
 // and dO are bf16 here (fp32 callers are converted by a pre-pass); O and the
 // gradients use the caller's dtype.
+//
+// With rotary embeddings (ROPE) q and k are the rotated ones; the gradients with
+// respect to them are carried back through the rotation (its transpose) in the
+// dQ and dK/dV epilogues, where a lane holds rows d and d + D/2 of its query or
+// key in accumulator blocks m and m + D/64.
 
 #include <hip/hip_runtime.h>
 
@@ -53,7 +58,26 @@ struct BwdParams {
   int hq, hkv, sumT;
   float scale;
   float scale_log2;
+  const int32_t* pos;      // ROPE: position of every flat token
+  const double* inv_freq;  // ROPE: [D/2]
 };
+
+// Inverse rotary rotation of one lane's gradient row held in 32x32 accumulator
+// layout: v[m][r] is element 32m + 8(r/4) + 4hf + r%4 of the row.
+template <int D, typename Row>
+__device__ __forceinline__ void rope_grad_rows(Row (&v)[D / 32], const double* inv_freq, int pos, int hf) {
+  constexpr int HM = D / 64;  // accumulator blocks per half
+#pragma unroll
+  for (int m = 0; m < HM; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      float cs, sn;
+      rope_cos_sin(pos, inv_freq[32 * m + 8 * (r >> 2) + 4 * hf + (r & 3)], cs, sn);
+      const float g1 = v[m][r], g2 = v[m + HM][r];
+      v[m][r] = g1 * cs + g2 * sn;
+      v[m + HM][r] = g2 * cs - g1 * sn;
+    }
+}
 
 // ---------------------------------------------------------------------------
 // delta = rowsum(dO * O)
@@ -115,7 +139,7 @@ struct DkdvSmem {
   };
 };
 
-template <int D, typename TO>
+template <int D, typename TO, bool ROPE>
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   using Dma = TileDma<D, KBM / 8>;
   using KvDma = TileDma<D, KBN / 8>;
@@ -255,19 +279,20 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     if (qb == 0 && k_in_tile) {
       const float sc = pass == 0 ? p.scale : 1.f;
       TO* dst = pass == 0 ? dkrow : dvrow;
+      f32x16(&row)[D / 32] = pass == 0 ? acc_dk : acc_dv;  // summed and scaled in place
 #pragma unroll
       for (int m = 0; m < D / 32; ++m)
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4 v4;
+        for (int r = 0; r < 16; ++r) row[m][r] = (row[m][r] + red[(m * 16 + r) * 64 + lane]) * sc;
+      if constexpr (ROPE) {
+        if (pass == 0) rope_grad_rows<D>(row, p.inv_freq, p.pos[it.tok0 + j], hf);
+      }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int r = 4 * r4 + e;
-            const float a = pass == 0 ? acc_dk[m][r] : acc_dv[m][r];
-            v4[e] = (a + red[(m * 16 + r) * 64 + lane]) * sc;
-          }
-          store4<TO>(dst + 32 * m + 8 * r4 + 4 * hf, v4);
-        }
+      for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          store4<TO>(dst + 32 * m + 8 * r4 + 4 * hf,
+                     f32x4{row[m][4 * r4], row[m][4 * r4 + 1], row[m][4 * r4 + 2], row[m][4 * r4 + 3]});
     }
   }
 }
@@ -279,8 +304,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
 constexpr int QBN = kDqBlockN;  // 32 or 64
 constexpr int QKB = QBN / 32;   // 32-key blocks per tile
 
-template <int D, int NW, int NS, typename TO>
-__global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p) {
+template <int D, int NW, int NS, typename TO, bool ROPE>
+__global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdParams<TO> p) {
   constexpr int RPW = QBN / NW;
   using Dma = TileDma<D, RPW>;
   __shared__ __attribute__((aligned(1024))) __bf16 sKV[NS][2][QBN * D];
@@ -381,15 +406,19 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void bwd_dq_kernel(BwdParams<TO> p
   }
 
   if (!in_tile) return;
+  f32x16(&gq)[D / 32] = acc;
+#pragma unroll
+  for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) gq[m][r] *= p.scale;
+  if constexpr (ROPE) rope_grad_rows<D>(gq, p.inv_freq, p.pos[it.tok0 + i], hf);
   TO* row = p.dq + qrow * D;
 #pragma unroll
   for (int m = 0; m < D / 32; ++m)
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      f32x4 v4 = {acc[m][4 * r4] * p.scale, acc[m][4 * r4 + 1] * p.scale, acc[m][4 * r4 + 2] * p.scale,
-                  acc[m][4 * r4 + 3] * p.scale};
-      store4<TO>(row + 32 * m + 8 * r4 + 4 * hf, v4);
-    }
+    for (int r4 = 0; r4 < 4; ++r4)
+      store4<TO>(row + 32 * m + 8 * r4 + 4 * hf,
+                 f32x4{gq[m][4 * r4], gq[m][4 * r4 + 1], gq[m][4 * r4 + 2], gq[m][4 * r4 + 3]});
 }
 
 template <int D, typename TO>
@@ -415,6 +444,8 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   p.sumT = a.sumT;
   p.scale = a.scale;
   p.scale_log2 = a.scale * kLog2e;
+  p.pos = a.pos;
+  p.inv_freq = a.inv_freq;
   const int64_t n_rows = (int64_t)a.sumT * a.hq;
   if (n_rows == 0) return hipSuccess;
   {
@@ -427,15 +458,17 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dkdv", s);
-    hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO>), dim3((unsigned)((int64_t)a.n_kv_items * a.hkv)), dim3(512), 0, s,
-                       p);
+    const dim3 grid((unsigned)((int64_t)a.n_kv_items * a.hkv));
+    if (a.rope) hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, true>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, false>), grid, dim3(512), 0, s, p);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dq", s);
-    hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqStages, TO>), dim3((unsigned)((int64_t)a.n_dq_items * a.hq)), dim3(kDqWaves * 64), 0,
-                       s, p);
+    const dim3 grid((unsigned)((int64_t)a.n_dq_items * a.hq));
+    if (a.rope) hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqStages, TO, true>), grid, dim3(kDqWaves * 64), 0, s, p);
+    else hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqStages, TO, false>), grid, dim3(kDqWaves * 64), 0, s, p);
   }
   return hipGetLastError();
 }

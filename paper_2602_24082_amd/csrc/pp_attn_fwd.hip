@@ -21,6 +21,12 @@
 //
 // Q, K, V are bf16 (fp32 callers are converted by a pre-pass); O is written in
 // the caller's dtype.
+//
+// With rotary embeddings (ROPE), K arrives already rotated and each wave rotates
+// its queries in registers right after loading them: pair (j, j + D/2) of a
+// query row sits in the same lane (chunks c and c + D/32), so the rotation needs
+// no data exchange; the rotated rows are also written out when the caller asks
+// for them (the backward pass takes them as its q).
 
 #include <hip/hip_runtime.h>
 
@@ -47,10 +53,44 @@ struct FwdParams {
   int hq, hkv, sumT;
   float scale;
   float scale_log2;
+  const int32_t* pos;      // ROPE: position of every flat token
+  const double* inv_freq;  // ROPE: [D/2]
+  TO* q_rot;               // ROPE: rotated queries out, or null
 };
 
-template <int D, int NW, int NS, typename TO>
-__global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO> p) {
+// Rotates the query fragments of one lane (qf[c] holds elements 16c + 8hf .. +7
+// of its query row) by the query's position and, when asked, stores the rotated
+// row.  The products run in fp32; the fragments are rounded back to bf16.
+template <int D, typename TO>
+__device__ __forceinline__ void rope_query(bf16x8 (&qf)[D / 16], const FwdParams<TO>& p, int pos, int hf,
+                                           TO* q_rot_row) {
+  constexpr int HC = D / 32;  // chunks per half
+#pragma unroll
+  for (int c = 0; c < HC; ++c) {
+    float y1[8], y2[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float cs, sn;
+      rope_cos_sin(pos, p.inv_freq[16 * c + 8 * hf + e], cs, sn);
+      const float x1 = (float)qf[c][e], x2 = (float)qf[c + HC][e];
+      y1[e] = x1 * cs - x2 * sn;
+      y2[e] = x2 * cs + x1 * sn;
+    }
+    qf[c] = to_bf16x8(y1[0], y1[1], y1[2], y1[3], y1[4], y1[5], y1[6], y1[7]);
+    qf[c + HC] = to_bf16x8(y2[0], y2[1], y2[2], y2[3], y2[4], y2[5], y2[6], y2[7]);
+    if (q_rot_row) {
+      TO* a = q_rot_row + 16 * c + 8 * hf;
+      TO* b = a + D / 2;
+      store4<TO>(a, f32x4{y1[0], y1[1], y1[2], y1[3]});
+      store4<TO>(a + 4, f32x4{y1[4], y1[5], y1[6], y1[7]});
+      store4<TO>(b, f32x4{y2[0], y2[1], y2[2], y2[3]});
+      store4<TO>(b + 4, f32x4{y2[4], y2[5], y2[6], y2[7]});
+    }
+  }
+}
+
+template <int D, int NW, int NS, typename TO, bool ROPE>
+__global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(FwdParams<TO> p) {
   constexpr int RPW = BN / NW;  // tile rows each wave fetches
   using Dma = TileDma<D, RPW>;
   __shared__ __attribute__((aligned(1024))) __bf16 sKV[NS][2][BN * D];  // [stage][K/V][row*D]
@@ -81,6 +121,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_fwd_kernel(FwdParams<TO>
 #pragma unroll
   for (int c = 0; c < D / 16; ++c)
     qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
+  if constexpr (ROPE) {
+    if (in_tile) rope_query<D, TO>(qf, p, p.pos[it.tok0 + i], hf, p.q_rot ? p.q_rot + qrow * D : nullptr);
+  }
 
   const int64_t kv_stride = (int64_t)p.hkv * D;
   const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
@@ -245,11 +288,18 @@ hipError_t launch_fwd_t(const AttnFwdLaunch& a, hipStream_t s) {
   p.sumT = a.sumT;
   p.scale = a.scale;
   p.scale_log2 = a.scale * kLog2e;
+  p.pos = a.pos;
+  p.inv_freq = a.inv_freq;
+  p.q_rot = (TO*)a.q_rot;
   const int64_t blocks = (int64_t)a.n_items * a.hq;
   if (blocks == 0) return hipSuccess;
   TimingScope t("pp_attn_fwd", s);
-  hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdWaves, kFwdStages, TO>), dim3((unsigned)blocks),
-                     dim3(kFwdWaves * 64), 0, s, p);
+  if (a.rope)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdWaves, kFwdStages, TO, true>), dim3((unsigned)blocks),
+                       dim3(kFwdWaves * 64), 0, s, p);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<D, kFwdWaves, kFwdStages, TO, false>), dim3((unsigned)blocks),
+                       dim3(kFwdWaves * 64), 0, s, p);
   return hipGetLastError();
 }
 

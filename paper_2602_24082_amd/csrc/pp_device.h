@@ -270,6 +270,27 @@ __device__ __forceinline__ Item load_uniform(const Item* p) {
   return out;
 }
 
+// cos and sin of the rotary angle pos * inv_freq.  The angle is formed in fp64
+// and reduced there to r in [-pi/4, pi/4] plus a quadrant k (angle = k pi/2 + r),
+// so the result does not depend on the size of the position (an fp32 product of
+// a position near 8192 would already be off by ~5e-4 rad).  sin r and cos r are
+// their Taylor series through r^9 and r^10, evaluated in fp32 (truncation below
+// 2e-9 on the interval); the quadrant then permutes and negates them.
+__device__ __forceinline__ void rope_cos_sin(int pos, double inv_freq, float& c, float& s) {
+  const double a = (double)pos * inv_freq;
+  const double k = rint(a * 0.6366197723675814);  // 2 / pi
+  const float r = (float)fma(-k, 1.5707963267948966, a);
+  const float r2 = r * r;
+  const float sr = r * (1.f + r2 * (-1.f / 6 + r2 * (1.f / 120 + r2 * (-1.f / 5040 + r2 * (1.f / 362880)))));
+  const float cr =
+      1.f + r2 * (-0.5f + r2 * (1.f / 24 + r2 * (-1.f / 720 + r2 * (1.f / 40320 + r2 * (-1.f / 3628800)))));
+  const int q = (int)((int64_t)k & 3);
+  const float ss = (q & 1) ? cr : sr;
+  const float cc = (q & 1) ? sr : cr;
+  s = (q & 2) ? -ss : ss;
+  c = (q == 1 || q == 2) ? -cc : cc;
+}
+
 // Maps a linear workgroup index to (item, head).  Workgroups are dispatched to
 // the 8 XCDs round-robin (index % 8); when the head count is a multiple of 8 the
 // heads of one item are arranged so that each XCD receives a contiguous run of

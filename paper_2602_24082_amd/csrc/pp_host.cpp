@@ -285,6 +285,34 @@ void build_seg_lo(const Batch& bt, std::vector<int32_t>* out) {
     for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_start(r, t);
 }
 
+// Position ID of row-relative token t (Sec. 3.2: each token keeps the position
+// it has in its unpacked sequence): t in the prompt, P + j for token j of a
+// response, 0 for padding.
+int32_t token_position(const Row& r, int32_t t) {
+  const int32_t sid = seg_id(r, t);
+  if (sid == 0) return t;
+  if (sid > 0) return r.P + (t - r.off[sid - 1]);
+  return 0;
+}
+
+void build_positions(const Batch& bt, std::vector<int32_t>* out) {
+  out->assign(bt.sumT, 0);
+  for (const Row& r : bt.rows)
+    for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = token_position(r, t);
+}
+
+// Rotary frequencies base^(-2j/d), j < d/2, in fp64.
+void build_inv_freq(int d, float base, std::vector<double>* out) {
+  out->resize(d / 2);
+  for (int j = 0; j < d / 2; ++j) (*out)[j] = std::pow((double)base, -2.0 * j / d);
+}
+
+pp_status check_rope_base(float base) {
+  if (!(base > 0.f) || !std::isfinite(base))
+    return fail(PP_ERR_INVALID_ARGUMENT, "rope_base must be a finite value > 0, got %g", (double)base);
+  return PP_OK;
+}
+
 struct LPlan {
   std::vector<LogitRowItem> rows;
   std::vector<int32_t> labels;     // flat position of each label token
@@ -447,7 +475,7 @@ struct FwdPlan {
   QPlan q;
   std::vector<int32_t> seg_lo;
   Layout lay;
-  size_t r_seg, r_items, r_kt;
+  size_t r_seg, r_items, r_kt, r_pos, r_freq;
   CastRegions cast;
 };
 
@@ -458,6 +486,10 @@ void plan_fwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, FwdPlan* 
   p->r_seg = p->lay.add(p->seg_lo.size() * 4);
   p->r_items = p->lay.add(p->q.items.size() * sizeof(QTileItem));
   p->r_kt = p->lay.add(p->q.ktiles.size() * sizeof(KTileEntry));
+  // the rotary variant also stages positions and frequencies (last, so that
+  // the plain forward copies only the prefix before them)
+  p->r_pos = p->lay.add((size_t)bt.sumT * 4);
+  p->r_freq = p->lay.add((size_t)d / 2 * 8);
   p->lay.meta_bytes = p->lay.total;
   if (dtype == PP_FP32) {
     p->cast.on = true;
@@ -472,7 +504,7 @@ struct BwdPlan {
   std::vector<KTileItem> kv;
   std::vector<int32_t> seg_lo;
   Layout lay;
-  size_t r_seg, r_dq_items, r_dq_kt, r_kv_items, r_delta;
+  size_t r_seg, r_dq_items, r_dq_kt, r_kv_items, r_pos, r_freq, r_delta;
   CastRegions cast;
 };
 
@@ -485,6 +517,8 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
   p->r_dq_items = p->lay.add(p->dq.items.size() * sizeof(QTileItem));
   p->r_dq_kt = p->lay.add(p->dq.ktiles.size() * sizeof(KTileEntry));
   p->r_kv_items = p->lay.add(p->kv.size() * sizeof(KTileItem));
+  p->r_pos = p->lay.add((size_t)bt.sumT * 4);
+  p->r_freq = p->lay.add((size_t)d / 2 * 8);
   p->lay.meta_bytes = p->lay.total;
   p->r_delta = p->lay.add((size_t)hq * bt.sumT * 4);
   if (dtype == PP_FP32) {
@@ -712,16 +746,30 @@ pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, in
   return PP_OK;
 }
 
-pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
-                      float scale, const void* q, const void* k, const void* v, void* o,
-                      float* lse, void* ws, size_t ws_bytes, void* hip_stream) {
+}  // extern "C"
+
+namespace pp {
+namespace {
+
+// Rotary arguments of the fused attention entry points (null for the plain ones).
+struct RopeArgs {
+  float base;
+  void* q_rot;        // forward: rotated queries out (may be null)
+  void* k_rot;        // forward: rotated keys out (required)
+};
+
+pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
+                        const void* q, const void* k, const void* v, void* o, float* lse, const RopeArgs* rope,
+                        void* ws, size_t ws_bytes, void* hip_stream) {
   Batch bt;
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (rope && (st = check_rope_base(rope->base)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
+  if (bt.sumT > 0 && rope && !rope->k_rot) return fail(PP_ERR_INVALID_ARGUMENT, "k_rot must be non-NULL");
   FwdPlan p;
   plan_fwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lay.total)
@@ -734,8 +782,34 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
   img.put(p.lay.regions[p.r_items], p.q.items.data(), p.q.items.size() * sizeof(QTileItem));
   img.put(p.lay.regions[p.r_kt], p.q.ktiles.data(), p.q.ktiles.size() * sizeof(KTileEntry));
+  std::vector<int32_t> pos;
+  std::vector<double> freq;
+  if (rope) {
+    build_positions(bt, &pos);
+    build_inv_freq(head_dim, rope->base, &freq);
+    img.put(p.lay.regions[p.r_pos], pos.data(), pos.size() * 4);
+    img.put(p.lay.regions[p.r_freq], freq.data(), freq.size() * 8);
+  }
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
   hipError_t e;
+  const int32_t* d_pos = (const int32_t*)at(ws, p.lay, p.r_pos);
+  const double* d_freq = (const double*)at(ws, p.lay, p.r_freq);
+  if (rope) {
+    // keys are rotated once, in the caller's dtype, into k_rot; the queries are
+    // rotated inside the attention kernel
+    RopeLaunch r{};
+    r.x = k;
+    r.y = rope->k_rot;
+    r.pos = d_pos;
+    r.inv_freq = d_freq;
+    r.sumT = bt.sumT;
+    r.heads = hkv;
+    r.head_dim = head_dim;
+    r.inverse = false;
+    r.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+    if ((e = launch_rope(r, s)) != hipSuccess) return hip_fail(e, "rotary embedding launch");
+    k = rope->k_rot;
+  }
   if (p.cast.on) {
     // the kernels read bf16: round fp32 inputs once (nearest even)
     void* qb = at(ws, p.lay, p.cast.q);
@@ -765,20 +839,27 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   a.sumT = bt.sumT;
   a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
   a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  if (rope) {
+    a.rope = true;
+    a.pos = d_pos;
+    a.inv_freq = d_freq;
+    a.q_rot = rope->q_rot;
+  }
   e = launch_attn_fwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention forward launch");
   return PP_OK;
 }
 
-pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
-                      float scale, const void* q, const void* k, const void* v, const void* o,
-                      const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
-                      size_t ws_bytes, void* hip_stream) {
+pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
+                        const void* q, const void* k, const void* v, const void* o, const float* lse,
+                        const void* dout, void* dq, void* dk, void* dv, const float* rope_base, void* ws,
+                        size_t ws_bytes, void* hip_stream) {
   Batch bt;
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (rope_base && (st = check_rope_base(*rope_base)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
   BwdPlan p;
@@ -794,6 +875,14 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   img.put(p.lay.regions[p.r_dq_items], p.dq.items.data(), p.dq.items.size() * sizeof(QTileItem));
   img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * sizeof(KTileEntry));
   img.put(p.lay.regions[p.r_kv_items], p.kv.data(), p.kv.size() * sizeof(KTileItem));
+  std::vector<int32_t> pos;
+  std::vector<double> freq;
+  if (rope_base) {
+    build_positions(bt, &pos);
+    build_inv_freq(head_dim, *rope_base, &freq);
+    img.put(p.lay.regions[p.r_pos], pos.data(), pos.size() * 4);
+    img.put(p.lay.regions[p.r_freq], freq.data(), freq.size() * 8);
+  }
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
   hipError_t e;
   const void* dout_bf = dout;
@@ -836,8 +925,119 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
   a.sumT = bt.sumT;
   a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
   a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  if (rope_base) {
+    a.rope = true;
+    a.pos = (const int32_t*)at(ws, p.lay, p.r_pos);
+    a.inv_freq = (const double*)at(ws, p.lay, p.r_freq);
+  }
   e = launch_attn_bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention backward launch");
+  return PP_OK;
+}
+
+// Workspace of pp_rope: positions then frequencies.
+struct RopePlan {
+  Layout lay;
+  size_t r_pos, r_freq;
+};
+
+void plan_rope(const Batch& bt, int d, RopePlan* p) {
+  p->lay = Layout();
+  p->r_pos = p->lay.add((size_t)bt.sumT * 4);
+  p->r_freq = p->lay.add((size_t)d / 2 * 8);
+  p->lay.meta_bytes = p->lay.total;
+}
+
+pp_status check_rope_dim(int d) {
+  if (d < 8 || d > 1024 || d % 8)
+    return fail(PP_ERR_UNSUPPORTED, "rotary head_dim %d not supported (a multiple of 8 in [8, 1024])", d);
+  return PP_OK;
+}
+
+}  // namespace
+}  // namespace pp
+
+extern "C" {
+
+pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      float scale, const void* q, const void* k, const void* v, void* o,
+                      float* lse, void* ws, size_t ws_bytes, void* hip_stream) {
+  return attn_fwd_impl(desc, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, nullptr, ws, ws_bytes, hip_stream);
+}
+
+pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      float scale, const void* q, const void* k, const void* v, const void* o,
+                      const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
+                      size_t ws_bytes, void* hip_stream) {
+  return attn_bwd_impl(desc, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, dout, dq, dk, dv, nullptr, ws,
+                       ws_bytes, hip_stream);
+}
+
+pp_status pp_attn_fwd_rope(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                           float scale, float rope_base, const void* q, const void* k, const void* v,
+                           void* o, float* lse, void* q_rot, void* k_rot, void* ws, size_t ws_bytes,
+                           void* hip_stream) {
+  RopeArgs r{rope_base, q_rot, k_rot};
+  return attn_fwd_impl(desc, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, &r, ws, ws_bytes, hip_stream);
+}
+
+pp_status pp_attn_bwd_rope(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                           float scale, float rope_base, const void* q_rot, const void* k_rot,
+                           const void* v, const void* o, const float* lse, const void* dout, void* dq,
+                           void* dk, void* dv, void* ws, size_t ws_bytes, void* hip_stream) {
+  return attn_bwd_impl(desc, dtype, hq, hkv, head_dim, scale, q_rot, k_rot, v, o, lse, dout, dq, dk, dv,
+                       &rope_base, ws, ws_bytes, hip_stream);
+}
+
+pp_status pp_rope_workspace_size(const pp_pack_desc* desc, int head_dim, size_t* bytes) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_rope_dim(head_dim)) != PP_OK) return st;
+  if (!bytes) return fail(PP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  RopePlan p;
+  plan_rope(bt, head_dim, &p);
+  *bytes = p.lay.total;
+  return PP_OK;
+}
+
+pp_status pp_rope(const pp_pack_desc* desc, pp_dtype dtype, int heads, int head_dim, float rope_base,
+                  int inverse, const void* x, void* y, void* ws, size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if ((st = check_rope_dim(head_dim)) != PP_OK) return st;
+  if ((st = check_rope_base(rope_base)) != PP_OK) return st;
+  if (heads < 1) return fail(PP_ERR_INVALID_ARGUMENT, "heads must be >= 1");
+  if (bt.sumT > 0 && (!x || !y)) return fail(PP_ERR_INVALID_ARGUMENT, "x and y must be non-NULL");
+  RopePlan p;
+  plan_rope(bt, head_dim, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "rope needs %zu workspace bytes, got %zu", p.lay.total, ws_bytes);
+  if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (bt.sumT == 0) return PP_OK;
+  hipStream_t s = (hipStream_t)hip_stream;
+  std::vector<int32_t> pos;
+  std::vector<double> freq;
+  build_positions(bt, &pos);
+  build_inv_freq(head_dim, rope_base, &freq);
+  MetaImage img;
+  img.put(p.lay.regions[p.r_pos], pos.data(), pos.size() * 4);
+  img.put(p.lay.regions[p.r_freq], freq.data(), freq.size() * 8);
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  RopeLaunch r{};
+  r.x = x;
+  r.y = y;
+  r.pos = (const int32_t*)at(ws, p.lay, p.r_pos);
+  r.inv_freq = (const double*)at(ws, p.lay, p.r_freq);
+  r.sumT = bt.sumT;
+  r.heads = heads;
+  r.head_dim = head_dim;
+  r.inverse = inverse != 0;
+  r.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
+  const hipError_t e = launch_rope(r, s);
+  if (e != hipSuccess) return hip_fail(e, "rotary embedding launch");
   return PP_OK;
 }
 
@@ -1131,12 +1331,7 @@ pp_status pp_pack_export(const pp_pack_desc* desc, int block_q, int block_k, int
     for (int32_t t = 0; t < r.T; ++t) {
       const int32_t sid = seg_id(r, t);
       if (segment_ids) segment_ids[r.tok0 + t] = sid;
-      if (position_ids) {
-        int32_t pos = 0;
-        if (sid == 0) pos = t;
-        else if (sid > 0) pos = r.P + (t - r.off[sid - 1]);
-        position_ids[r.tok0 + t] = pos;
-      }
+      if (position_ids) position_ids[r.tok0 + t] = token_position(r, t);
     }
     if (tile_class) {
       for (int32_t q0 = 0; q0 < r.T; q0 += block_q)

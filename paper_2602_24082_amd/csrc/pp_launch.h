@@ -41,6 +41,13 @@ struct AttnFwdLaunch {
   int sumT;
   float scale;
   int dtype;
+  // rotary embedding of the queries in the kernel's prologue (k is already
+  // rotated): position of every flat token, inv_freq[head_dim/2], and where the
+  // rotated queries go (dtype `dtype`, may be null)
+  bool rope = false;
+  const int32_t* pos = nullptr;
+  const double* inv_freq = nullptr;
+  void* q_rot = nullptr;
 };
 hipError_t launch_attn_fwd(const AttnFwdLaunch& a, hipStream_t s);
 
@@ -67,8 +74,25 @@ struct AttnBwdLaunch {
   int sumT;
   float scale;
   int dtype;
+  // q and k are rotated; dq and dk are rotated back before they are stored
+  bool rope = false;
+  const int32_t* pos = nullptr;
+  const double* inv_freq = nullptr;
 };
 hipError_t launch_attn_bwd(const AttnBwdLaunch& a, hipStream_t s);
+
+// y = rotation of x by each token's position ([sumT, heads, head_dim], dtype);
+// inverse rotates by the negative angle.  y may equal x.
+struct RopeLaunch {
+  const void* x;
+  void* y;
+  const int32_t* pos;
+  const double* inv_freq;
+  int sumT, heads, head_dim;
+  bool inverse;
+  int dtype;
+};
+hipError_t launch_rope(const RopeLaunch& a, hipStream_t s);
 
 struct LogprobLaunch {
   const void* logits;

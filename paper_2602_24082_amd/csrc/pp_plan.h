@@ -37,6 +37,14 @@ namespace pp {
 #ifndef PP_FWD_BLOCK_N
 #define PP_FWD_BLOCK_N 64
 #endif
+// minimum waves per SIMD the forward and dQ kernels are compiled for (this
+// caps their registers at 512 / n per lane)
+#ifndef PP_FWD_MIN_WAVES
+#define PP_FWD_MIN_WAVES (8 / PP_FWD_WAVES)
+#endif
+#ifndef PP_DQ_MIN_WAVES
+#define PP_DQ_MIN_WAVES (8 / PP_DQ_WAVES)
+#endif
 #ifndef PP_DQ_BLOCK_N
 #define PP_DQ_BLOCK_N 64
 #endif

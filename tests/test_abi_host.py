@@ -230,3 +230,33 @@ def test_workspace_sizes_grow_with_batch():
     a = binding.pp_workspace_size(small, 4, 4, 64, 1000, logprob=True)
     b = binding.pp_workspace_size(big, 32, 8, 128, 128256, logprob=True)
     assert all(x > 0 for x in a) and all(y >= x for x, y in zip(a, b))
+
+
+def test_rope_argument_checks():
+    """Rotary entry points: bad base, head_dim, NULLs and workspace come back as
+    error codes before anything is enqueued."""
+    L = binding.lib()
+    fake = ctypes.c_void_p(16)
+    d, keep = _raw_desc([0, 12], [4], [2], [4, 7], [3, 3], 2)
+    n = ctypes.c_size_t(0)
+    assert L.pp_rope_workspace_size(ctypes.byref(d), 128, ctypes.byref(n)) == 0 and n.value >= 12 * 4 + 64 * 8
+    assert L.pp_rope_workspace_size(ctypes.byref(d), 12, ctypes.byref(n)) == 3
+    assert L.pp_rope_workspace_size(ctypes.byref(d), 128, None) == 1
+    rope = lambda dt=0, H=2, hd=128, base=10000.0, x=fake, y=fake, nb=1 << 30: L.pp_rope(
+        ctypes.byref(d), dt, H, hd, base, 0, x, y, fake, nb, None)
+    assert rope(hd=100) == 3
+    assert rope(base=0.0) == 1 and rope(base=-5.0) == 1 and rope(base=float("inf")) == 1
+    assert rope(H=0) == 1 and rope(dt=9) == 1
+    assert rope(x=None) == 1 and rope(y=None) == 1
+    assert rope(nb=1) == 4
+    fwd = lambda base=10000.0, qr=fake, kr=fake, hd=128, nb=1 << 30: L.pp_attn_fwd_rope(
+        ctypes.byref(d), 0, 4, 2, hd, 0.0, base, fake, fake, fake, fake, fake, qr, kr, fake, nb, None)
+    assert fwd(base=0.0) == 1
+    assert fwd(kr=None) == 1
+    assert fwd(hd=96) == 3
+    assert fwd(nb=1) == 4
+    bwd = lambda base=10000.0, nb=1 << 30: L.pp_attn_bwd_rope(
+        ctypes.byref(d), 0, 4, 2, 128, 0.0, base, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake, nb,
+        None)
+    assert bwd(base=float("nan")) == 1
+    assert bwd(nb=1) == 4

@@ -73,6 +73,52 @@ def test_fullsize_dpo_chain_attention():
     _attention_sample(4, group=0)
 
 
+def _attention_rope_sample(cfg_index, group, base):
+    """The fused rotary path on a whole benchmarked batch; the oracle recomputes
+    one row and one kv-head group on the bf16-rounded rotations the kernels
+    attend with, and carries the gradients back through the exact rotation."""
+    cfg = wl.CONFIGS[cfg_index]
+    pack = wl.config_pack(cfg)
+    seed = wl.tensor_seed(cfg.index, 0)
+    q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, seed, torch.bfloat16, DEV)
+    o, lse, q_rot, k_rot = pp.pp_attn_fwd_rope(pack, q, k, v, base)
+    dq, dk, dv = pp.pp_attn_bwd_rope(pack, q_rot, k_rot, v, o, lse, do, base)
+    torch.cuda.synchronize()
+    b = int(np.argmin(pack.row_lengths()))
+    r0, r1 = int(pack.row_start[b]), int(pack.row_start[b + 1])
+    G = cfg.hq // cfg.hkv
+    hs = slice(group * G, (group + 1) * G)
+    gs = slice(group, group + 1)
+    print(f"{cfg.name} rope base {base}: row {b} T={r1 - r0}, kv-head {group}", flush=True)
+    sub = lambda x, s: x[r0:r1, s].double().cpu().numpy()
+    args = _row_pack(pack, b).oracle_args()
+    qr = orc.pack_rope(*args, sub(q, hs), base)
+    kr = orc.pack_rope(*args, sub(k, gs), base)
+    for got, ref in ((sub(q_rot, hs), qr), (sub(k_rot, gs), kr)):
+        assert (np.abs(got - ref) <= 2.0 ** -8 * np.abs(ref) + 4e-6 * np.abs(ref).max()).all()
+    to_bf = lambda a: torch.from_numpy(a).to(torch.bfloat16).double().numpy()
+    qb, kb = to_bf(qr), to_bf(kr)
+    O_ref, L_ref = orc.attn_fwd(*args, qb, kb, sub(v, gs))
+    dqr, dkr, dv_r = orc.attn_bwd(*args, qb, kb, sub(v, gs), sub(do, hs))
+    assert np.abs(sub(o, hs) - O_ref).max() <= 1e-2
+    assert np.abs(lse[hs, r0:r1].double().cpu().numpy() - L_ref).max() <= 1e-2
+    for name, got, ref in (("dq", sub(dq, hs), orc.pack_rope(*args, dqr, base, inverse=True)),
+                           ("dk", sub(dk, gs), orc.pack_rope(*args, dkr, base, inverse=True)),
+                           ("dv", sub(dv, gs), dv_r)):
+        err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+        assert err <= 2e-2, (name, err)
+    for t in (o, lse, dq, dk, dv, q_rot, k_rot):
+        assert torch.isfinite(t).all()
+
+
+def test_fullsize_llama3_8b_attention_rope():
+    _attention_rope_sample(1, group=2, base=500000.0)
+
+
+def test_fullsize_long_prefix_attention_rope():
+    _attention_rope_sample(3, group=4, base=1000000.0)
+
+
 def _compact_response(pack, b, k, logits, tokens):
     """One response as its own pack: the predicting row P-1 then the rows that
     predict tokens 2..L, with the response's labels (the oracle's index rule
