@@ -368,7 +368,6 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
     __syncthreads();
     if (t + NS - 1 < n_tiles) issue(t + NS - 1);
     if (cls == kWaveSkip) continue;
-    const bool need_mask = cls == kWaveMasked;
     const __bf16* sK = sKV[t % NS][0];
     const __bf16* sV = sKV[t % NS][1];
 
@@ -382,16 +381,22 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
 #pragma unroll
       for (int c = 0; c < D / 16; ++c) dp[kb] = mfma32(lds_row8<D>(sV, kb * 32 + ln, 2 * c + hf), df[c], dp[kb]);
     }
-    const int jb = k0 + 4 * hf;
+    // dS^T = P^T (dP^T - delta) with P^T = exp2(S^T scale log2e - lse log2e) on
+    // the visible pairs.  One branch-free loop serves every kind of block (two
+    // copies would push the kernel past 256 registers): on a full block lim and
+    // hole pass every key, on a causal block the hole test does (hole 0).
+    const bool need_mask = cls != kWaveFull;
+    const int lim = need_mask ? hi - k0 - 4 * hf : 64;
+    const unsigned hole_t = cls == kWaveMasked ? hole : 0u;
+    const int jp = k0 + 4 * hf - it.P;
 #pragma unroll
     for (int kb = 0; kb < QKB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int jj = jb + kb * 32 + 8 * (r >> 2) + (r & 3);
-        const bool vis = (!need_mask) | ((jj <= hi) & ((unsigned)(jj - it.P) >= hole));
+        const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
+        const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole_t);
         const float e = fast_exp2(fmaf(s[kb][r], p.scale_log2, -lse2));
-        const float pr = vis ? e : 0.f;
-        dp[kb][r] = pr * (dp[kb][r] - dlt);
+        dp[kb][r] = (vis ? e : 0.f) * (dp[kb][r] - dlt);
       }
     bf16x8 db[2 * QKB];
 #pragma unroll

@@ -161,7 +161,6 @@ __global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(Fwd
     __syncthreads();  // tile t landed for every wave; the stage of tile t-1 is free
     if (t + NS - 1 < n_tiles) issue(t + NS - 1);
     if (cls == kWaveSkip) continue;
-    const bool need_mask = cls == kWaveMasked;
     const __bf16* sK = sKV[t % NS][0];
     const __bf16* sV = sKV[t % NS][1];
 
@@ -189,14 +188,23 @@ __global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(Fwd
         __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
       }
     }
-    if (need_mask) {
-      const int jb = k0 + 4 * hf;
+    if (cls == kWaveCausal) {
+      // only the causal edge cuts this block: key k0 + 4hf + off is visible
+      // iff off <= hi - k0 - 4hf
+      const int lim = hi - k0 - 4 * hf;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[kb][r] = (kb * 32 + 8 * (r >> 2) + (r & 3)) <= lim ? s[kb][r] : kNegInf;
+    } else if (cls == kWaveMasked) {
+      const int lim = hi - k0 - 4 * hf;
+      const int jp = k0 + 4 * hf - it.P;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int j = jb + kb * 32 + 8 * (r >> 2) + (r & 3);
-          const bool vis = (j <= hi) & ((unsigned)(j - it.P) >= hole);
+          const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
+          const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole);
           s[kb][r] = vis ? s[kb][r] : kNegInf;
         }
     }
@@ -206,7 +214,7 @@ __global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(Fwd
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+    mx = half_swap_max(mx) * c2;
     const bool raise = mx > m_ref + kRescaleSlack;
     if (wave_any(raise)) {
       const float m_new = raise ? mx : m_ref;
@@ -245,7 +253,7 @@ __global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(Fwd
   }
 
   if (!in_tile) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float l_tot = half_swap_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   TO* orow = p.o + qrow * D;
 #pragma unroll

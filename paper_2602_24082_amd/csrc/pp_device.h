@@ -230,6 +230,20 @@ __device__ __forceinline__ void wait_tile(int t, int n) {
   }
 }
 
+// max / sum of x and the value held by lane l ^ 32 (the other half of the
+// wave), through v_permlane32_swap: a VALU exchange of the two 32-lane halves
+// of two registers, with no LDS round trip.  Swapping x with itself leaves
+// r[0] = x of lane l & 31 and r[1] = x of lane (l & 31) + 32 in every lane.
+__device__ __forceinline__ float half_swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return a > b ? a : b;
+}
+__device__ __forceinline__ float half_swap_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ float wave_max(float x) {
   for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
   return x;
@@ -241,8 +255,10 @@ __device__ __forceinline__ float wave_sum(float x) {
 }
 
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedValu = 0x002;
 constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
+constexpr int kSchedTrans = 0x400;
 
 // Wave-wide any of a lane predicate, as a value the compiler knows is uniform
 // (so a branch on it does not make a loop divergent).

@@ -228,8 +228,14 @@ void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
           if (qa < qb) {
             const int64_t n = visible_pairs(r, qa, qb, k0, k1);
             // a key tile cut short by the row's end leaves lanes without a key: masked
-            if (n == (int64_t)(qb - qa) * BN) cls = kWaveFull;
-            else if (n > 0) cls = kWaveMasked;
+            if (n == (int64_t)(qb - qa) * BN) {
+              cls = kWaveFull;
+            } else if (n > 0) {
+              // the visible pairs are exactly the causal ones among real tokens:
+              // the mask reduces to j <= i
+              const int64_t causal = sum_ramp(qa, std::min(qb, r.valid), k0, std::min(k1, r.valid));
+              cls = n == causal ? kWaveCausal : kWaveMasked;
+            }
           }
           e.cls |= (uint32_t)cls << (2 * w);
         }

@@ -61,19 +61,24 @@ constexpr int kFwdBlockN = PP_FWD_BLOCK_N;  // keys per forward k-tile (32 or 64
 constexpr int kDqBlockM = 32 * kDqWaves;    // queries per dQ workgroup
 constexpr int kDqBlockN = PP_DQ_BLOCK_N;    // keys per dQ k-tile (32 or 64)
 constexpr int kBwdBlockN = 128;             // keys per dK/dV workgroup (8 waves: 4 key blocks x 2)
+
+
 constexpr int kBwdBlockM = 64;              // queries per dK/dV inner step
 
 // An entry of a query tile's key-tile list: the tile's first key (row-relative)
-// and, per 32-query wave of the query tile, a 2-bit class of the wave's block
-// of pairs against the key tile, worked out exactly on the host:
-//   kWaveSkip   no pair of the block is visible (the wave sits the tile out);
+// and, per 32-query block w of the query tile, a 2-bit class of the block's
+// pairs against the key tile, worked out exactly on the host:
+//   kWaveSkip   no pair of the block is visible (the block sits the tile out);
 //   kWaveFull   every pair is visible (no mask);
-//   kWaveMasked some pairs are visible (the mask is evaluated per element).
+//   kWaveMasked some pairs are visible (the full mask is evaluated per element);
+//   kWaveCausal some pairs are visible and they are exactly the causal ones
+//               (j <= i, both real tokens): the mask reduces to one compare.
+// Kernels that do not use the causal class treat it as masked (bit 1 set).
 struct KTileEntry {
   int32_t k0;
-  uint32_t cls;  // bits 2w, 2w+1: class of wave w
+  uint32_t cls;  // bits 2w, 2w+1: class of block w
 };
-constexpr int kWaveSkip = 0, kWaveFull = 1, kWaveMasked = 2;
+constexpr int kWaveSkip = 0, kWaveFull = 1, kWaveMasked = 2, kWaveCausal = 3;
 constexpr int kMaxClassWaves = 16;
 static_assert(kFwdWaves <= kMaxClassWaves && kDqWaves <= kMaxClassWaves, "2 class bits per wave");
 
