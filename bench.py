@@ -125,18 +125,28 @@ class Attn:
                        dk=self.dk, dv=self.dv, ws=self.ws_b)
 
 
+def median_time(fn, iters=10, warmup=3, reps=5):
+    """Median over `reps` repetitions of the mean time of `iters` back-to-back
+    calls (HIP events on the stream): one repetition disturbed by a host stall
+    that lets the GPU run dry does not move the result."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(iters):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        times.append(s.elapsed_time(e) / iters)
+    return float(np.median(times))
+
+
 def time_attention(pack, hq, hkv, d, dev, iters=10, warmup=3):
     a = Attn(pack, hq, hkv, d, 977, dev)
-    for _ in range(warmup):
-        a.run()
-    torch.cuda.synchronize()
-    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    s.record()
-    for _ in range(iters):
-        a.run()
-    e.record()
-    torch.cuda.synchronize()
-    ms = s.elapsed_time(e) / iters
+    ms = median_time(a.run, iters, warmup)
     del a
     torch.cuda.empty_cache()
     return ms
@@ -313,16 +323,7 @@ def rope_leg(pack, cfg, seed, dev, base, iters=10):
         pp.pp_rope(pack, a.dk, base, inverse=True, out=a.dk, ws=ws_r)
 
     def timed(fn):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s.record()
-        for _ in range(iters):
-            fn()
-        e.record()
-        torch.cuda.synchronize()
-        return s.elapsed_time(e) / iters
+        return median_time(fn, iters)
 
     t_plain = timed(a.run)
     t_fused = timed(fused)
@@ -330,7 +331,9 @@ def rope_leg(pack, cfg, seed, dev, base, iters=10):
     # the standalone rotation of q alone: bytes = read + write of q (bf16)
     pp.pp_timing_reset()
     pp.pp_timing_enable(True)
-    timed(lambda: pp.pp_rope(pack, a.q, base, out=q_rot, ws=ws_r))
+    for _ in range(iters):
+        pp.pp_rope(pack, a.q, base, out=q_rot, ws=ws_r)
+    torch.cuda.synchronize()
     pp.pp_timing_enable(False)
     kr = pp.pp_timing_get()["pp_rope"]
     q_bytes = pack.total_tokens * hq * d * 2 * 2
@@ -432,7 +435,8 @@ def main():
     pp.pp_timing_enable(False)
     kern = pp.pp_timing_get()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    attn_ms = sum(a.elapsed_time(b) for a, b in attn_ev) / args.steps
+    attn_each = [a.elapsed_time(b) for a, b in attn_ev]
+    attn_ms = sum(attn_each) / args.steps
     loss_val = float(loss.item())
 
     U = useful_pairs(pack)
@@ -554,6 +558,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "attn_ms_per_step": round(attn_ms, 4),
+        "attn_ms_median_step": round(float(np.median(attn_each)), 4),
         "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "higher_is_better": True,
         "scaling": "weak",
