@@ -293,6 +293,141 @@ __global__ __launch_bounds__(kLpThreads) void logprob_bwd_kernel(LogprobBwdLaunc
   }
 }
 
+// Log-prob backward with the row held in registers: one 512-thread workgroup
+// per flat logit row.  A needed row is read from HBM once -- thread t loads the
+// 16-byte vectors t, t + 512, ... (up to kLpbVecs of them) -- its logsumexp is
+// formed from the registers (thread maximum, then thread sum of exponentials,
+// then a fixed-order workgroup combine), and the gradient is computed from the
+// same registers and streamed out, so each row costs one read and one write of
+// HBM (the two-pass kernel above reads it twice).  Rows that predict nothing
+// are streamed zeros.  Used when the row's 16-byte vectors fit
+// (vocab <= 512 * kLpbVecs * elements per vector) and rows are 16-byte aligned.
+constexpr int kLpbThreads = 512;
+constexpr int kLpbVecs = 40;
+
+template <int R>
+__device__ __forceinline__ void opaque(u32x4 (&u)[R]) {
+#pragma unroll
+  for (int j = 0; j < R; ++j) asm volatile("" : "+v"(u[j]));
+}
+
+template <typename T>
+__global__ __launch_bounds__(kLpbThreads) void logprob_bwd_reg_kernel(LogprobBwdLaunch a) {
+  constexpr int N = Vec16<T>::N;
+  constexpr int NW = kLpbThreads / 64;
+  const int64_t r = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int vocab = a.vocab;
+  const int nvec = vocab / N;  // vocab % N == 0 here
+  u32x4* ov = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.dlogits) + r * (int64_t)vocab);
+  const int item = a.row_item[r];
+  if (item < 0) {
+#pragma unroll
+    for (int j = 0; j < kLpbVecs; ++j) {
+      const int vi = j * kLpbThreads + tid;
+      if (vi < nvec) __builtin_nontemporal_store(u32x4{0, 0, 0, 0}, ov + vi);
+    }
+    return;
+  }
+  const u32x4* xv = reinterpret_cast<const u32x4*>(reinterpret_cast<const T*>(a.logits) + r * (int64_t)vocab);
+  u32x4 u[kLpbVecs];
+#pragma unroll
+  for (int j = 0; j < kLpbVecs; ++j) {
+    const int vi = j * kLpbThreads + tid;
+    u[j] = vi < nvec ? __builtin_nontemporal_load(xv + vi) : u32x4{0, 0, 0, 0};
+  }
+  const LogitRowItem it = a.rows[item];
+  __shared__ int s_y[kMaxRowLabels];
+  __shared__ float s_g[kMaxRowLabels];
+  __shared__ float s_m[NW], s_s[NW];
+  __shared__ float s_c, s_lse;
+  __shared__ int s_bad;
+  const int cnt = it.label_cnt;
+  if (tid == 0) s_bad = 0;
+  __syncthreads();
+  for (int j = tid; j < cnt; j += kLpbThreads) {
+    const int32_t y = a.tokens[a.labels[it.label_off + j]];
+    s_y[j] = y;
+    s_g[j] = a.dseq[a.label_out[it.label_off + j]];
+    if (y < 0 || y >= vocab) s_bad = 1;
+  }
+  // logsumexp of the row from the registers
+  float m = kNegInf;
+#pragma unroll
+  for (int j = 0; j < kLpbVecs; ++j) {
+    if (j * kLpbThreads + tid < nvec) {
+      float f[N];
+      Vec16<T>::unpack(u[j], f);
+#pragma unroll
+      for (int e = 0; e < N; ++e) m = fmaxf(m, f[e]);
+    }
+  }
+  // the packed vectors count as rewritten here, so each pass below unpacks
+  // them again instead of keeping the whole row live as floats
+  opaque(u);
+  float s = 0.f;
+  if (m != kNegInf) {
+    const float ml = m * kLog2e;
+#pragma unroll
+    for (int j = 0; j < kLpbVecs; ++j) {
+      if (j * kLpbThreads + tid < nvec) {
+        float f[N];
+        Vec16<T>::unpack(u[j], f);
+#pragma unroll
+        for (int e = 0; e < N; ++e) s += fast_exp2(fmaf(f[e], kLog2e, -ml));
+      }
+    }
+  }
+  MaxSum acc = {m, s};
+  for (int off = 32; off > 0; off >>= 1) {
+    MaxSum o;
+    o.m = __shfl_xor(acc.m, off, 64);
+    o.s = __shfl_xor(acc.s, off, 64);
+    acc = combine(acc, o);
+  }
+  const int wave = tid >> 6, lane = tid & 63;
+  if (lane == 0) {
+    s_m[wave] = acc.m;
+    s_s[wave] = acc.s;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    MaxSum w = {s_m[0], s_s[0]};
+    for (int i = 1; i < NW; ++i) w = combine(w, MaxSum{s_m[i], s_s[i]});
+    s_lse = w.m + logf(w.s);
+    float c = 0.f;
+    for (int j = 0; j < cnt; ++j) c += s_g[j];
+    s_c = c;
+  }
+  __syncthreads();
+  const float c = s_c;
+  const float lse2 = s_lse * kLog2e;
+  const bool bad = s_bad != 0;
+  opaque(u);
+#pragma unroll
+  for (int j = 0; j < kLpbVecs; ++j) {
+    const int vi = j * kLpbThreads + tid;
+    if (vi < nvec) {
+      float f[N];
+      Vec16<T>::unpack(u[j], f);
+#pragma unroll
+      for (int e = 0; e < N; ++e) f[e] = -c * fast_exp2(fmaf(f[e], kLog2e, -lse2));
+      for (int l = 0; l < cnt; ++l) {
+        const int d = s_y[l] - vi * N;
+        if ((unsigned)d < (unsigned)N) {
+#pragma unroll
+          for (int e = 0; e < N; ++e) f[e] += (e == d) ? s_g[l] : 0.f;
+        }
+      }
+      if (bad) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) f[e] = __builtin_nanf("");
+      }
+      __builtin_nontemporal_store(Pack16<T>::pack(f), ov + vi);
+    }
+  }
+}
+
 // One wave per (row, response) slot; lane l sums tokens l, l+64, ... in order,
 // then a fixed butterfly, so the result does not depend on scheduling.
 __global__ __launch_bounds__(256) void segsum_kernel(const float* __restrict__ tok,
@@ -396,6 +531,20 @@ hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s) {
 hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s) {
   if (a.sumT <= 0) return hipSuccess;
   TimingScope t("pp_logprob_bwd", s);
+  const int esz = a.dtype == kBF16 ? 2 : 4;
+  const int per_vec = 16 / esz;
+  // the one-read kernel needs every row to start on a 16-byte boundary and to
+  // fit in the workgroup's registers
+  const bool fits = a.vocab % per_vec == 0 && a.vocab <= kLpbThreads * kLpbVecs * per_vec &&
+                    (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0 &&
+                    (reinterpret_cast<uintptr_t>(a.dlogits) & 15) == 0;
+  if (fits) {
+    if (a.dtype == kBF16)
+      hipLaunchKernelGGL(logprob_bwd_reg_kernel<__bf16>, dim3(a.sumT), dim3(kLpbThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL(logprob_bwd_reg_kernel<float>, dim3(a.sumT), dim3(kLpbThreads), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.dtype == kBF16)
     hipLaunchKernelGGL(logprob_bwd_kernel<__bf16>, dim3(a.sumT), dim3(kLpThreads), 0, s, a);
   else
