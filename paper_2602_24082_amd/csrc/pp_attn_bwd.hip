@@ -2,7 +2,7 @@
 //
 // Three deterministic passes (no atomics):
 //
-//   bwd_prep   delta_i = dO_i . O_i  (fp32, [hq, sumT])
+//   bwd_prep   delta_i = dO_i . O_i and -lse_i log2(e)  (fp32, [hq, sumT])
 //   bwd_dkdv   key-major: one workgroup = one 128-key tile of one kv-head and
 //              eight waves; waves w and w+4 own keys 32*(w%4) .. +31 and take the
 //              two 32-query halves of each 64-query step (two waves per SIMD).
@@ -14,7 +14,7 @@
 //              response's queries, so the shared prompt's dK/dV gather all K
 //              responses' contributions in one place.  Per step (S = Q K^T,
 //              lane = key):
-//                P  = exp2(S*scale*log2e - lse_i*log2e) (masked)
+//                P  = exp2(S*scale*log2e - lse_i*log2e) (masked; -lse*log2e from bwd_prep)
 //                dP = dO V^T,  dS = P (dP - delta_i)
 //                dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T by transposed LDS reads)
 //   bwd_dq     query-major, like the forward (lane = query):
@@ -51,10 +51,12 @@ struct BwdParams {
   TO* dk;
   TO* dv;
   float* delta;
+  float* nlse2;  // -LSE * log2(e), written next to delta
   const QTileItem* dq_items;
   const KTileEntry* dq_ktiles;
   const KTileItem* kv_items;
   const int32_t* seg_lo;
+  const int32_t* seg_hi;
   int hq, hkv, sumT;
   float scale;
   float scale_log2;
@@ -80,7 +82,8 @@ __device__ __forceinline__ void rope_grad_rows(Row (&v)[D / 32], const double* i
 }
 
 // ---------------------------------------------------------------------------
-// delta = rowsum(dO * O)
+// delta = rowsum(dO * O), and -LSE log2(e) in the layout the dK/dV kernel
+// stages (the exponent of P is then one fma away from S)
 // ---------------------------------------------------------------------------
 
 template <int D, typename TO>
@@ -102,6 +105,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t 
     const int64_t t = row / p.hq;
     const int h = (int)(row % p.hq);
     p.delta[(int64_t)h * p.sumT + t] = acc;
+    p.nlse2[(int64_t)h * p.sumT + t] = -p.lse[(int64_t)h * p.sumT + t] * kLog2e;
   }
 }
 
@@ -113,22 +117,21 @@ constexpr int KBN = kBwdBlockN;  // 128 keys per workgroup
 constexpr int KBM = kBwdBlockM;  // 64 queries per step
 
 // One pipeline stage of the dK/dV kernel: the step's Q and dO tiles and the
-// per-query scalars, all filled by DMA.
+// per-query -LSE log2(e) and delta, all filled by DMA.
 template <int D>
 struct DkdvStage {
   __bf16 q[KBM * D];
   __bf16 dout[KBM * D];
-  float lse[KBM];
+  float nlse2[KBM];
   float delta[KBM];
-  int seg_lo[KBM];
-  int spare[KBM];  // receives the fourth wave's info DMA (keeps per-wave counts equal)
 };
 
 // Waves w and w+4 own the same 32 keys and take the
 // two 32-query halves of every 64-query step, so each SIMD runs two waves.  K
 // and V stay in LDS for the whole workgroup (B operands read by row), which
 // keeps a wave within 256 registers; the two halves' dK/dV partials are added
-// through LDS at the end.
+// through LDS at the end.  K, V (64 KB) and two stages (2 x 33 KB) fill most
+// of the 160 KB of LDS, so the next step's tiles are fetched one step ahead.
 template <int D>
 struct DkdvSmem {
   __bf16 k[KBN * D];
@@ -143,8 +146,6 @@ template <int D, typename TO, bool ROPE>
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   using Dma = TileDma<D, KBM / 8>;
   using KvDma = TileDma<D, KBN / 8>;
-  constexpr int NS = 2;
-  constexpr int PER_STEP = 2 * Dma::N + 1;
   __shared__ __attribute__((aligned(1024))) DkdvSmem<D> sm;
 
   const int item_idx = blockIdx.x / p.hkv;
@@ -163,11 +164,14 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   const int j = it.k0 + kb * 32 + ln;
   const bool k_in_tile = j < it.k_end;
   const int64_t krow = (int64_t)(it.tok0 + j) * p.hkv + g;
-  const unsigned jP = (unsigned)(j - it.P);
   const int wk0 = it.k0 + kb * 32;
   const int wk1 = min(min(it.k_end, it.valid), wk0 + 32);
   const bool wave_live = wk0 < wk1;
   const int qlim = min(it.q_end, it.valid);
+  // Key j is visible from query i iff j <= i < seg_hi(j) (the row's first
+  // padding position for a prompt key, the end of its own response for a
+  // response key, 0 for padding): with i = j + u that is u < span as unsigned.
+  const unsigned span = k_in_tile ? (unsigned)max(0, min(qlim, p.seg_hi[it.tok0 + j]) - j) : 0u;
 
   const int nq = it.q_end - it.q_begin;
   const int nsteps = (nq + KBM - 1) / KBM;
@@ -188,22 +192,26 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     }
   }
 
+  // Steps run head by head, each over the tile's 64-query steps; the fetch
+  // (one step ahead) and the compute keep their own counters.
   Dma dma;
   dma.init(wave * (KBM / 8), q_stride, lane);
+  int f_hh = 0, f_stp = 0;  // next step to fetch
   auto issue = [&](int n) {
-    DkdvStage<D>& sg = sm.st[n % NS];
-    const int hh = n / nsteps, stp = n - hh * nsteps;
-    const int head = g * G + hh;
-    const int qs = it.q_begin + stp * KBM;
+    DkdvStage<D>& sg = sm.st[n & 1];
+    const int head = g * G + f_hh;
+    const int qs = it.q_begin + f_stp * KBM;
     const int rows = min(KBM, it.q_end - qs);
     const int64_t t0 = (int64_t)it.tok0 + qs;
     dma.issue(sg.q, p.q + (t0 * p.hq + head) * D, rows);
     dma.issue(sg.dout, p.dout + (t0 * p.hq + head) * D, rows);
     const int64_t tq = t0 + min(lane, rows - 1);
-    if (wave == 0) dma_dword(sg.lse, p.lse + (int64_t)head * p.sumT + tq);
+    if (wave == 0) dma_dword(sg.nlse2, p.nlse2 + (int64_t)head * p.sumT + tq);
     else if (wave == 1) dma_dword(sg.delta, p.delta + (int64_t)head * p.sumT + tq);
-    else if (wave == 2) dma_dword(sg.seg_lo, p.seg_lo + tq);
-    else dma_dword(sg.spare, p.seg_lo + tq);
+    if (++f_stp == nsteps) {
+      f_stp = 0;
+      ++f_hh;
+    }
   };
   if (n_iter > 0) issue(0);
 
@@ -214,50 +222,108 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     acc_dv[m] = f32x16{};
   }
 
+  int qs = it.q_begin - KBM;  // first query of the current step
   for (int n = 0; n < n_iter; ++n) {
-    wait_tile<NS, PER_STEP>(n, n_iter);  // the K/V tile (issued first) has landed as well
-    __syncthreads();
+    qs = qs + KBM == it.q_begin + nsteps * KBM ? it.q_begin : qs + KBM;
+    wait_vmem<0>();  // this wave's part of step n (and, at n = 0, of K and V) has landed
+    __syncthreads();  // ... for every wave; the stage of step n-1 is free
     if (n + 1 < n_iter) issue(n + 1);
     if (!wave_live) continue;
-    const DkdvStage<D>& sg = sm.st[n % NS];
-    const int qs = it.q_begin + (n % nsteps) * KBM;
+    const DkdvStage<D>& sg = sm.st[n & 1];
     const int qb0 = qs + qb * 32;
     if (qb0 >= qlim) continue;
     if (min(qb0 + 31, qlim - 1) < wk0) continue;
 
+    // S = Q K^T and dP = dO V^T over D/16 chunks; the four fragments of chunk
+    // c + 1 are read while chunk c's two MFMAs run (the scheduling groups keep
+    // the compiler from bunching the reads)
     f32x16 s = f32x16{}, dp = f32x16{};
+    {
+      constexpr int NC = D / 16;
+      bf16x8 fq[2], fk[2], fo[2], fv[2];
+      auto load = [&](int c, int b) {
+        fq[b] = lds_row8<D>(sg.q, qb * 32 + ln, 2 * c + hf);
+        fk[b] = lds_row8<D>(sm.k, kb * 32 + ln, 2 * c + hf);
+        fo[b] = lds_row8<D>(sg.dout, qb * 32 + ln, 2 * c + hf);
+        fv[b] = lds_row8<D>(sm.v, kb * 32 + ln, 2 * c + hf);
+      };
+      load(0, 0);
 #pragma unroll
-    for (int c = 0; c < D / 16; ++c) {
-      s = mfma32(lds_row8<D>(sg.q, qb * 32 + ln, 2 * c + hf), lds_row8<D>(sm.k, kb * 32 + ln, 2 * c + hf), s);
-      dp = mfma32(lds_row8<D>(sg.dout, qb * 32 + ln, 2 * c + hf), lds_row8<D>(sm.v, kb * 32 + ln, 2 * c + hf), dp);
+      for (int c = 0; c < NC; ++c) {
+        if (c + 1 < NC) load(c + 1, (c + 1) & 1);
+        s = mfma32(fq[c & 1], fk[c & 1], s);
+        dp = mfma32(fo[c & 1], fv[c & 1], dp);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        if (c + 1 < NC) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+      }
+    }
+    // masked pairs get S = -inf (so P = dS = 0); a block whose 32 x 32 pairs
+    // are all visible skips the test
+    const int u_first = qb0 - j;  // query - key of the half's first query
+    if (wave_any(!(u_first >= 0 && (unsigned)(u_first + 31) < span))) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const unsigned u0 = (unsigned)(u_first + 8 * r4 + 4 * hf);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s[4 * r4 + e] = u0 + e < span ? s[4 * r4 + e] : kNegInf;
+      }
     }
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       const int il = qb * 32 + 8 * r4 + 4 * hf;
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sg.lse[il]);
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sg.nlse2[il]);
       const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sg.delta[il]);
-      typedef int i32x4 __attribute__((ext_vector_type(4)));
-      const i32x4 o4 = *reinterpret_cast<const i32x4*>(&sg.seg_lo[il]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = 4 * r4 + e;
-        const int qi = qs + il + e;
-        const unsigned hole = o4[e] > it.P ? (unsigned)(o4[e] - it.P) : 0u;
-        const bool vis = (j <= qi) & (qi < qlim) & (jP >= hole);
-        const float ex = fast_exp2(fmaf(s[r], p.scale_log2, -l4[e] * kLog2e));
-        const float pr = vis ? ex : 0.f;
+        const float pr = fast_exp2(fmaf(s[r], p.scale_log2, l4[e]));
         s[r] = pr;
         dp[r] = pr * (dp[r] - d4[e]);
       }
     }
     const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
     const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
+    // dV^T += dO^T P and dK^T += Q^T dS: product n is block m = n / 4 of dV (n
+    // even) or dK (n odd) over query rows 0-15 (n % 4 < 2) or 16-31 of the
+    // half; the transposed fragments are read PD products ahead (PD 0: each
+    // right before its MFMA, the compiler's schedule)
+    {
+      constexpr int NI = 4 * (D / 32), PD = PP_DKDV_TR_PREFETCH;
+      auto frag = [&](int n) {
+        return lds_tr8<D>((n & 1) ? sg.q : sg.dout, qb * 32 + 16 * ((n >> 1) & 1), 32 * (n >> 2), lane);
+      };
+      if constexpr (PD == 0) {
 #pragma unroll
-    for (int m = 0; m < D / 32; ++m) {
-      acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
-      acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32, 32 * m, lane), db0, acc_dk[m]);
-      acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
-      acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
+        for (int m = 0; m < D / 32; ++m) {
+          acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
+          acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32, 32 * m, lane), db0, acc_dk[m]);
+          acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
+          acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
+        }
+      } else {
+      bf16x8 a[PD + 1];
+#pragma unroll
+      for (int n = 0; n < PD; ++n) a[n] = frag(n);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) a[(n + PD) % (PD + 1)] = frag(n + PD);
+        const int m = n >> 2, t = n & 3;
+        const bf16x8& b = t == 0 ? pb0 : t == 1 ? db0 : t == 2 ? pb1 : db1;
+        if (t & 1) acc_dk[m] = mfma32(a[n % (PD + 1)], b, acc_dk[m]);
+        else acc_dv[m] = mfma32(a[n % (PD + 1)], b, acc_dv[m]);
+      }
+#pragma unroll
+      for (int n = 0; n < PD; ++n) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      }
+      }
     }
   }
 
@@ -329,7 +395,7 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
   const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
   const unsigned hole = (real && lo > it.P) ? (unsigned)(lo - it.P) : 0u;
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
-  const float lse2 = real ? p.lse[(int64_t)head * p.sumT + it.tok0 + i] * kLog2e : 0.f;
+  const float nlse2 = real ? -p.lse[(int64_t)head * p.sumT + it.tok0 + i] * kLog2e : 0.f;
   const float dlt = real ? p.delta[(int64_t)head * p.sumT + it.tok0 + i] : 0.f;
   bf16x8 qf[D / 16], df[D / 16];
 #pragma unroll
@@ -371,43 +437,95 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
     const __bf16* sK = sKV[t % NS][0];
     const __bf16* sV = sKV[t % NS][1];
 
+    // S^T = K Q^T and dP^T = V dO^T, one 32x32 block each per 32 keys: the K
+    // and V fragments are read PD ahead of the MFMA that consumes them
     f32x16 s[QKB], dp[QKB];
+    {
+      constexpr int NC = D / 16, NI = 2 * QKB * NC, PD = PP_DQ_PREFETCH;
+      // fragment n: key block n / (2 NC), K (first NC) or V (next NC), chunk n % NC
+      auto frag = [&](int n) {
+        return lds_row8<D>(((n / NC) & 1) ? sV : sK, (n / (2 * NC)) * 32 + ln, 2 * (n % NC) + hf);
+      };
+      bf16x8 a[PD + 1];
 #pragma unroll
-    for (int kb = 0; kb < QKB; ++kb) {
-      s[kb] = f32x16{};
-      dp[kb] = f32x16{};
+      for (int kb = 0; kb < QKB; ++kb) {
+        s[kb] = f32x16{};
+        dp[kb] = f32x16{};
+      }
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) s[kb] = mfma32(lds_row8<D>(sK, kb * 32 + ln, 2 * c + hf), qf[c], s[kb]);
+      for (int n = 0; n < PD; ++n) a[n] = frag(n);
 #pragma unroll
-      for (int c = 0; c < D / 16; ++c) dp[kb] = mfma32(lds_row8<D>(sV, kb * 32 + ln, 2 * c + hf), df[c], dp[kb]);
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) a[(n + PD) % (PD + 1)] = frag(n + PD);
+        const int kb = n / (2 * NC), c = n % NC;
+        if ((n / NC) & 1) dp[kb] = mfma32(a[n % (PD + 1)], df[c], dp[kb]);
+        else s[kb] = mfma32(a[n % (PD + 1)], qf[c], s[kb]);
+      }
+#pragma unroll
+      for (int n = 0; n < PD; ++n) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      }
     }
     // dS^T = P^T (dP^T - delta) with P^T = exp2(S^T scale log2e - lse log2e) on
-    // the visible pairs.  One branch-free loop serves every kind of block (two
-    // copies would push the kernel past 256 registers): on a full block lim and
-    // hole pass every key, on a causal block the hole test does (hole 0).
-    const bool need_mask = cls != kWaveFull;
-    const int lim = need_mask ? hi - k0 - 4 * hf : 64;
-    const unsigned hole_t = cls == kWaveMasked ? hole : 0u;
-    const int jp = k0 + 4 * hf - it.P;
+    // the visible pairs: a block that is not fully visible first sets S^T of
+    // its masked pairs to -inf (one test covers the causal and the general
+    // class: on a causal block the hole is empty).
+    if (cls != kWaveFull) {
+      const int lim = hi - k0 - 4 * hf;
+      const unsigned hole_t = cls == kWaveMasked ? hole : 0u;
+      const int jp = k0 + 4 * hf - it.P;
+#pragma unroll
+      for (int kb = 0; kb < QKB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
+          const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole_t);
+          s[kb][r] = vis ? s[kb][r] : kNegInf;
+        }
+    }
 #pragma unroll
     for (int kb = 0; kb < QKB; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
-        const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole_t);
-        const float e = fast_exp2(fmaf(s[kb][r], p.scale_log2, -lse2));
-        dp[kb][r] = (vis ? e : 0.f) * (dp[kb][r] - dlt);
-      }
+      for (int r = 0; r < 16; ++r)
+        dp[kb][r] = fast_exp2(fmaf(s[kb][r], p.scale_log2, nlse2)) * (dp[kb][r] - dlt);
     bf16x8 db[2 * QKB];
 #pragma unroll
     for (int kb = 0; kb < QKB; ++kb) {
       db[2 * kb] = acc_half_to_bf16(dp[kb], 0);
       db[2 * kb + 1] = acc_half_to_bf16(dp[kb], 1);
     }
+    // dQ^T += K^T dS^T: product n is block m = n % (D/32) over keys 16 ch ..
+    // +15, ch = n / (D/32); the transposed K fragments are read PD ahead (PD 0:
+    // each right before its MFMA)
+    {
+      constexpr int NM = D / 32, NI = 2 * QKB * NM, PD = PP_DQ_TR_PREFETCH;
+      auto frag = [&](int n) { return lds_tr8<D>(sK, 16 * (n / NM), 32 * (n % NM), lane); };
+      if constexpr (PD == 0) {
 #pragma unroll
-    for (int ch = 0; ch < 2 * QKB; ++ch)
+        for (int ch = 0; ch < 2 * QKB; ++ch)
 #pragma unroll
-      for (int m = 0; m < D / 32; ++m) acc[m] = mfma32(lds_tr8<D>(sK, 16 * ch, 32 * m, lane), db[ch], acc[m]);
+          for (int m = 0; m < NM; ++m) acc[m] = mfma32(lds_tr8<D>(sK, 16 * ch, 32 * m, lane), db[ch], acc[m]);
+      } else {
+      bf16x8 a[PD + 1];
+#pragma unroll
+      for (int n = 0; n < PD; ++n) a[n] = frag(n);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) a[(n + PD) % (PD + 1)] = frag(n + PD);
+        acc[n % NM] = mfma32(a[n % (PD + 1)], db[n / NM], acc[n % NM]);
+      }
+#pragma unroll
+      for (int n = 0; n < PD; ++n) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+#pragma unroll
+      for (int n = 0; n < NI; ++n) {
+        if (n + PD < NI) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      }
+      }
+    }
   }
 
   if (!in_tile) return;
@@ -440,10 +558,12 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   p.dk = (TO*)a.dk;
   p.dv = (TO*)a.dv;
   p.delta = a.delta;
+  p.nlse2 = a.nlse2;
   p.dq_items = a.dq_items;
   p.dq_ktiles = a.dq_ktiles;
   p.kv_items = a.kv_items;
   p.seg_lo = a.seg_lo;
+  p.seg_hi = a.seg_hi;
   p.hq = a.hq;
   p.hkv = a.hkv;
   p.sumT = a.sumT;

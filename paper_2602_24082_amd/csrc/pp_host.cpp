@@ -291,6 +291,22 @@ void build_seg_lo(const Batch& bt, std::vector<int32_t>* out) {
     for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_start(r, t);
 }
 
+// One past the last query that can see key t (row-relative): a prompt key is
+// seen by every later real token, a response key only by its own response's
+// later tokens (Sec. 3.2), a padding key by nothing.
+inline int32_t seg_end(const Row& r, int32_t t) {
+  if (t < r.P) return r.valid;
+  for (int k = 0; k < r.K; ++k)
+    if (r.off[k] <= t && t < r.off[k] + r.len[k]) return r.off[k] + r.len[k];
+  return 0;
+}
+
+void build_seg_hi(const Batch& bt, std::vector<int32_t>* out) {
+  out->assign(bt.sumT, 0);
+  for (const Row& r : bt.rows)
+    for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_end(r, t);
+}
+
 // Position ID of row-relative token t (Sec. 3.2: each token keeps the position
 // it has in its unpacked sequence): t in the prompt, P + j for token j of a
 // response, 0 for padding.
@@ -508,9 +524,9 @@ void plan_fwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, FwdPlan* 
 struct BwdPlan {
   QPlan dq;
   std::vector<KTileItem> kv;
-  std::vector<int32_t> seg_lo;
+  std::vector<int32_t> seg_lo, seg_hi;
   Layout lay;
-  size_t r_seg, r_dq_items, r_dq_kt, r_kv_items, r_pos, r_freq, r_delta;
+  size_t r_seg, r_seg_hi, r_dq_items, r_dq_kt, r_kv_items, r_pos, r_freq, r_delta, r_nlse2;
   CastRegions cast;
 };
 
@@ -518,8 +534,10 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
   build_qplan(bt, kDqBlockM, kDqBlockN, &p->dq);
   build_kplan(bt, kBwdBlockN, &p->kv);
   build_seg_lo(bt, &p->seg_lo);
+  build_seg_hi(bt, &p->seg_hi);
   p->lay = Layout();
   p->r_seg = p->lay.add(p->seg_lo.size() * 4);
+  p->r_seg_hi = p->lay.add(p->seg_hi.size() * 4);
   p->r_dq_items = p->lay.add(p->dq.items.size() * sizeof(QTileItem));
   p->r_dq_kt = p->lay.add(p->dq.ktiles.size() * sizeof(KTileEntry));
   p->r_kv_items = p->lay.add(p->kv.size() * sizeof(KTileItem));
@@ -527,6 +545,7 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
   p->r_freq = p->lay.add((size_t)d / 2 * 8);
   p->lay.meta_bytes = p->lay.total;
   p->r_delta = p->lay.add((size_t)hq * bt.sumT * 4);
+  p->r_nlse2 = p->lay.add((size_t)hq * bt.sumT * 4);
   if (dtype == PP_FP32) {
     p->cast.on = true;
     p->cast.q = p->lay.add((size_t)bt.sumT * hq * d * 2);
@@ -878,6 +897,7 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   hipStream_t s = (hipStream_t)hip_stream;
   MetaImage img;
   img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
+  img.put(p.lay.regions[p.r_seg_hi], p.seg_hi.data(), p.seg_hi.size() * 4);
   img.put(p.lay.regions[p.r_dq_items], p.dq.items.data(), p.dq.items.size() * sizeof(QTileItem));
   img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * sizeof(KTileEntry));
   img.put(p.lay.regions[p.r_kv_items], p.kv.data(), p.kv.size() * sizeof(KTileItem));
@@ -919,12 +939,14 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   a.dk = dk;
   a.dv = dv;
   a.delta = (float*)at(ws, p.lay, p.r_delta);
+  a.nlse2 = (float*)at(ws, p.lay, p.r_nlse2);
   a.dq_items = (const QTileItem*)at(ws, p.lay, p.r_dq_items);
   a.dq_ktiles = (const KTileEntry*)at(ws, p.lay, p.r_dq_kt);
   a.n_dq_items = (int)p.dq.items.size();
   a.kv_items = (const KTileItem*)at(ws, p.lay, p.r_kv_items);
   a.n_kv_items = (int)p.kv.size();
   a.seg_lo = (const int32_t*)at(ws, p.lay, p.r_seg);
+  a.seg_hi = (const int32_t*)at(ws, p.lay, p.r_seg_hi);
   a.hq = hq;
   a.hkv = hkv;
   a.head_dim = head_dim;

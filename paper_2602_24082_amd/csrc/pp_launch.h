@@ -64,12 +64,14 @@ struct AttnBwdLaunch {
   void* dk;
   void* dv;
   float* delta;              // [hq, sumT] scratch
+  float* nlse2;              // [hq, sumT] scratch: -LSE * log2(e)
   const QTileItem* dq_items;
   const KTileEntry* dq_ktiles;
   int n_dq_items;
   const KTileItem* kv_items;
   int n_kv_items;
   const int32_t* seg_lo;
+  const int32_t* seg_hi;  // per token: one past the last query that sees it as a key
   int hq, hkv, head_dim;
   int sumT;
   float scale;
