@@ -91,21 +91,24 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t 
   constexpr int LPR = D / 8;      // lanes per (token, head) row
   constexpr int RPB = 256 / LPR;  // rows per block
   const int tid = threadIdx.x;
+  // rows run head-major (row = h * sumT + t), the layout of lse, delta and
+  // nlse2, so a block's per-row values are contiguous; each O / dO row is a
+  // whole D-element run
   const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;
   const int part = tid % LPR;
+  const int64_t h = row / p.sumT, t = row - h * p.sumT;
+  const int64_t src = (t * p.hq + h) * D + part * 8;
   float acc = 0.f;
   if (row < n_rows) {
-    const TO* a = p.dout_o + row * D + part * 8;
-    const TO* b = p.o + row * D + part * 8;
+    const TO* a = p.dout_o + src;
+    const TO* b = p.o + src;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc += (float)a[e] * (float)b[e];
   }
   for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
   if (row < n_rows && part == 0) {
-    const int64_t t = row / p.hq;
-    const int h = (int)(row % p.hq);
-    p.delta[(int64_t)h * p.sumT + t] = acc;
-    p.nlse2[(int64_t)h * p.sumT + t] = -p.lse[(int64_t)h * p.sumT + t] * kLog2e;
+    p.delta[row] = acc;
+    p.nlse2[row] = -p.lse[row] * kLog2e;
   }
 }
 
