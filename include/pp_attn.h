@@ -25,6 +25,10 @@
  *   every pointer named "host" is host memory read before the call returns.
  *   The library allocates no device memory; it keeps a small ring of pinned host
  *   staging buffers for plan metadata, freed when the library is unloaded.
+ *   Tensor arguments of the attention and rotary entry points (q, k, v, o, dout,
+ *   dq, dk, dv, q_rot, k_rot, x, y) must be 16-byte aligned, lse 4-byte aligned
+ *   (rows move in 16-byte vectors); a misaligned pointer is rejected with
+ *   PP_ERR_INVALID_ARGUMENT.  Allocations from hipMalloc or torch qualify.
  * Streams.  All device work is enqueued on `hip_stream` (a hipStream_t; NULL
  *   means the null stream) in call order; no entry point synchronises the device.
  * Errors.  Arguments are validated on the host before anything is enqueued; a
@@ -113,7 +117,7 @@ pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, in
  * head_dim in {64, 128}; hq % hkv == 0.
  * scale <= 0 selects 1/sqrt(head_dim).
  * Errors: PP_ERR_UNSUPPORTED for another head_dim; PP_ERR_INVALID_ARGUMENT for
- * null pointers or bad head counts; PP_ERR_BAD_LAYOUT for a bad descriptor;
+ * null or misaligned pointers or bad head counts; PP_ERR_BAD_LAYOUT for a bad descriptor;
  * PP_ERR_WORKSPACE_TOO_SMALL if ws_bytes is below pp_workspace_size's fwd. */
 pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                       float scale, const void* q, const void* k, const void* v, void* o,

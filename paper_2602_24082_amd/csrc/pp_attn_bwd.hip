@@ -86,29 +86,44 @@ __device__ __forceinline__ void rope_grad_rows(Row (&v)[D / 32], const double* i
 // stages (the exponent of P is then one fma away from S)
 // ---------------------------------------------------------------------------
 
+constexpr int kPrepRowsPerThread = 4;
+
 template <int D, typename TO>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t n_rows) {
   constexpr int LPR = D / 8;      // lanes per (token, head) row
-  constexpr int RPB = 256 / LPR;  // rows per block
+  constexpr int RPB = 256 / LPR;  // rows per block and pass
+  constexpr int RPT = kPrepRowsPerThread;
+  typedef TO vec8 __attribute__((ext_vector_type(8)));
   const int tid = threadIdx.x;
+  const int part = tid % LPR;
   // rows run head-major (row = h * sumT + t), the layout of lse, delta and
   // nlse2, so a block's per-row values are contiguous; each O / dO row is a
-  // whole D-element run
-  const int64_t row = (int64_t)blockIdx.x * RPB + tid / LPR;
-  const int part = tid % LPR;
-  const int64_t h = row / p.sumT, t = row - h * p.sumT;
-  const int64_t src = (t * p.hq + h) * D + part * 8;
-  float acc = 0.f;
-  if (row < n_rows) {
-    const TO* a = p.dout_o + src;
-    const TO* b = p.o + src;
+  // whole D-element run.  A thread's RPT rows are loaded before any is summed.
+  const int64_t row0 = (int64_t)blockIdx.x * RPB * RPT + tid / LPR;
+  vec8 a[RPT], b[RPT];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc += (float)a[e] * (float)b[e];
+  for (int k = 0; k < RPT; ++k) {
+    const int64_t row = row0 + k * RPB;
+    if (row < n_rows) {
+      const int64_t h = row / p.sumT, t = row - h * p.sumT;
+      const int64_t src = (t * p.hq + h) * D + part * 8;
+      a[k] = *reinterpret_cast<const vec8*>(p.dout_o + src);
+      b[k] = *reinterpret_cast<const vec8*>(p.o + src);
+    }
   }
-  for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-  if (row < n_rows && part == 0) {
-    p.delta[row] = acc;
-    p.nlse2[row] = -p.lse[row] * kLog2e;
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int64_t row = row0 + k * RPB;
+    float acc = 0.f;
+    if (row < n_rows) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc += (float)a[k][e] * (float)b[k][e];
+    }
+    for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (row < n_rows && part == 0) {
+      p.delta[row] = acc;
+      p.nlse2[row] = -p.lse[row] * kLog2e;
+    }
   }
 }
 
@@ -577,7 +592,7 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   const int64_t n_rows = (int64_t)a.sumT * a.hq;
   if (n_rows == 0) return hipSuccess;
   {
-    constexpr int RPB = 256 / (D / 8);
+    constexpr int RPB = 256 / (D / 8) * kPrepRowsPerThread;
     TimingScope t("pp_attn_bwd_prep", s);
     hipLaunchKernelGGL((bwd_prep_kernel<D, TO>), dim3((unsigned)((n_rows + RPB - 1) / RPB)), dim3(256), 0, s,
                        p, n_rows);

@@ -783,6 +783,11 @@ struct RopeArgs {
   void* k_rot;        // forward: rotated keys out (required)
 };
 
+// The kernels move tensor rows in 16-byte vectors (and DMA them into LDS in
+// 16-byte chunks), so every tensor argument must start on a 16-byte boundary.
+inline bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15) == 0; }
+inline bool aligned4(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 3) == 0; }
+
 pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
                         const void* q, const void* k, const void* v, void* o, float* lse, const RopeArgs* rope,
                         void* ws, size_t ws_bytes, void* hip_stream) {
@@ -795,6 +800,9 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
   if (bt.sumT > 0 && rope && !rope->k_rot) return fail(PP_ERR_INVALID_ARGUMENT, "k_rot must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned4(lse) ||
+      (rope && (!aligned16(rope->k_rot) || !aligned16(rope->q_rot))))
+    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o (and q_rot, k_rot) must be 16-byte aligned, lse 4-byte aligned");
   FwdPlan p;
   plan_fwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lay.total)
@@ -887,6 +895,9 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   if (rope_base && (st = check_rope_base(*rope_base)) != PP_OK) return st;
   if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(dq) ||
+      !aligned16(dk) || !aligned16(dv) || !aligned4(lse))
+    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, dout, dq, dk and dv must be 16-byte aligned, lse 4-byte aligned");
   BwdPlan p;
   plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lay.total)
@@ -1039,6 +1050,7 @@ pp_status pp_rope(const pp_pack_desc* desc, pp_dtype dtype, int heads, int head_
   if ((st = check_rope_base(rope_base)) != PP_OK) return st;
   if (heads < 1) return fail(PP_ERR_INVALID_ARGUMENT, "heads must be >= 1");
   if (bt.sumT > 0 && (!x || !y)) return fail(PP_ERR_INVALID_ARGUMENT, "x and y must be non-NULL");
+  if (!aligned16(x) || !aligned16(y)) return fail(PP_ERR_INVALID_ARGUMENT, "x and y must be 16-byte aligned");
   RopePlan p;
   plan_rope(bt, head_dim, &p);
   if (ws_bytes < p.lay.total)

@@ -260,3 +260,36 @@ def test_rope_argument_checks():
         None)
     assert bwd(base=float("nan")) == 1
     assert bwd(nb=1) == 4
+
+
+def test_misaligned_tensors_rejected():
+    """Attention and rotary tensors must be 16-byte aligned (lse 4-byte): a
+    misaligned pointer comes back as PP_ERR_INVALID_ARGUMENT before anything is
+    enqueued."""
+    L = binding.lib()
+    ok, off8, off2 = ctypes.c_void_p(4096), ctypes.c_void_p(4096 + 8), ctypes.c_void_p(4096 + 2)
+    d, keep = _raw_desc([0, 12], [4], [2], [4, 7], [3, 3], 2)
+    nb = 1 << 30
+
+    def fwd(q=ok, k=ok, v=ok, o=ok, lse=ok):
+        return L.pp_attn_fwd(ctypes.byref(d), 0, 4, 2, 128, 0.0, q, k, v, o, lse, ok, nb, None)
+
+    for kw in ("q", "k", "v", "o"):
+        assert fwd(**{kw: off8}) == 1, kw
+    assert fwd(lse=off2) == 1
+    assert b"aligned" in L.pp_last_error()
+
+    def bwd(**kw):
+        a = dict(q=ok, k=ok, v=ok, o=ok, lse=ok, dout=ok, dq=ok, dk=ok, dv=ok)
+        a.update(kw)
+        return L.pp_attn_bwd(ctypes.byref(d), 0, 4, 2, 128, 0.0, a["q"], a["k"], a["v"], a["o"], a["lse"],
+                             a["dout"], a["dq"], a["dk"], a["dv"], ok, nb, None)
+
+    for kw in ("q", "k", "v", "o", "dout", "dq", "dk", "dv"):
+        assert bwd(**{kw: off8}) == 1, kw
+    assert bwd(lse=off2) == 1
+    rope = lambda x=ok, y=ok: L.pp_rope(ctypes.byref(d), 0, 2, 128, 10000.0, 0, x, y, ok, nb, None)
+    assert rope(x=off8) == 1 and rope(y=off8) == 1
+    fwd_r = lambda qr=ok, kr=ok: L.pp_attn_fwd_rope(ctypes.byref(d), 0, 4, 2, 128, 0.0, 10000.0, ok, ok, ok, ok, ok,
+                                                    qr, kr, ok, nb, None)
+    assert fwd_r(qr=off8) == 1 and fwd_r(kr=off8) == 1
