@@ -108,17 +108,18 @@ typedef __attribute__((address_space(3))) void lds_void;
 // read of each tile) -- which includes the prefetch of the NEXT tile and so
 // serialises the prefetch with half of the compute it should overlap.  The
 // kernels' own waits are exact; the "memory" clobber keeps the compiler from
-// moving LDS accesses across the statement, and M0 is set inside it.
+// moving LDS accesses across the statement.  The LDS base goes in as an M0
+// operand, so the compiler sets M0 itself and knows what it holds.
 __device__ __forceinline__ void lds_dma16(const void* src, const void* lds_dst) {
   const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_void*)lds_dst);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(base) : "memory", "m0");
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(base) : "memory");
 }
 
 // One 4-byte element per lane into LDS (lane l -> lds + 4*l): the per-query
 // scalars of a 64-query tile.  Issued like lds_dma16.
 __device__ __forceinline__ void dma_dword(void* lds, const void* src) {
   const unsigned base = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_void*)lds);
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(base) : "memory", "m0");
+  asm volatile("global_load_lds_dword %0, off" ::"v"(src), "{m0}"(base) : "memory");
 }
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
