@@ -299,6 +299,49 @@ def chain_sorting(dev, reps=1):
                       "config": {"workload": cfg.name, "vocab": V, "beta": cfg.beta}, "cells": cells}))
 
 
+def plan_leg(pack, cfg, seed, dev, layers=8):
+    """The reusable plan: the pack planned and staged once (pp_plan_create), then
+    attention fwd+bwd on it for several layers in a row (different q, k, v
+    would not change the work), against the same layers through the
+    self-contained pp_attn_fwd / pp_attn_bwd, which plan and copy metadata in
+    every call.  Reports per-layer times and the plan's own cost (host
+    planning time, GPU time of its one metadata copy)."""
+    hq, hkv, d = cfg.hq, cfg.hkv, cfg.head_dim
+    a = Attn(pack, hq, hkv, d, seed, dev)
+    ws_p = torch.empty(pp.pp_plan_workspace_size(pack, hq, hkv, d), dtype=torch.uint8, device=dev)
+    plan = pp.pp_plan_create(pack, hq, hkv, d, ws=ws_p, device=dev)
+
+    def planned():
+        for _ in range(layers):
+            pp.pp_attn_fwd_planned(plan, a.q, a.k, a.v, out=a.o, lse=a.lse)
+            pp.pp_attn_bwd_planned(plan, a.q, a.k, a.v, a.o, a.lse, a.do, dq=a.dq, dk=a.dk, dv=a.dv)
+
+    def self_contained():
+        for _ in range(layers):
+            a.run()
+
+    t_plan = median_time(planned, iters=3, warmup=2) / layers
+    t_self = median_time(self_contained, iters=3, warmup=2) / layers
+    host = []
+    for _ in range(10):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        p2 = pp.pp_plan_create(pack, hq, hkv, d, ws=ws_p, device=dev)
+        host.append((time.perf_counter() - t0) * 1e3)
+        pp.pp_plan_destroy(p2)
+    gpu_copy = median_time(lambda: pp.pp_plan_destroy(pp.pp_plan_create(pack, hq, hkv, d, ws=ws_p, device=dev)),
+                           iters=5, warmup=2)
+    pp.pp_plan_destroy(plan)
+    useful = 14 * d * hq * useful_pairs(pack)
+    return {"layers": layers, "planned_ms_per_layer": round(t_plan, 4),
+            "self_contained_ms_per_layer": round(t_self, 4),
+            "planned_useful_TFLOP_s": round(useful / (t_plan * 1e-3) / 1e12, 1),
+            "plan_create_host_ms": round(float(np.median(host)), 4),
+            "plan_create_stream_ms": round(gpu_copy, 4),
+            "note": "value stays on pp_attn_fwd/pp_attn_bwd (plan + copy inside every call); this leg reuses "
+                    "one staged plan across layers, as a model would"}
+
+
 def rope_leg(pack, cfg, seed, dev, base, iters=10):
     """Attention fwd+bwd with rotary embeddings on the packed position IDs: the
     fused entry points (queries rotated in the forward's prologue, dq and dk
@@ -537,6 +580,7 @@ def main():
     del hidden
 
     rope = rope_leg(pack, cfg, seed, dev, ROPE_BASE.get(cfg.hq, 500000.0))
+    plan = plan_leg(pack, cfg, seed, dev)
 
     comp = cost = losing = None
     if not args.no_comparator:
@@ -576,6 +620,7 @@ def main():
         "logprob_bwd": logprob_bwd,
         "rm_head": rm_head,
         "rope": rope,
+        "plan": plan,
         "kernels": kernels,
         "attention_rooflines": attn_roofs,
         "roofline": roof,

@@ -18,6 +18,9 @@
  *   pp_rope, pp_attn_fwd_rope, pp_attn_bwd_rope
  *                   rotary position embedding on the packed position IDs
  *                   (Sec. 3.2), alone or fused into attention
+ *   pp_plan_create, pp_attn_fwd_planned, pp_attn_bwd_planned
+ *                   the same attention on a plan built once per packed batch
+ *                   and reused (e.g. by every layer of a model)
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -181,6 +184,59 @@ pp_status pp_attn_bwd_rope(const pp_pack_desc* desc, pp_dtype dtype, int hq, int
                            float scale, float rope_base, const void* q_rot, const void* k_rot,
                            const void* v, const void* o, const float* lse, const void* dout, void* dq,
                            void* dk, void* dv, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Reusable plans (the Plan step of the packed path, Sec. 3.2).  Every pp_attn_*
+ * call above plans the pack on the host and copies the plan's metadata into its
+ * workspace before its kernels run.  A model applies attention to the same
+ * packed batch in every layer, so the plan can be built once per batch instead:
+ *
+ *   pp_plan_workspace_size(desc, ...)           -> bytes for the plan's workspace
+ *   pp_plan_create(desc, ..., ws, stream, &pl)  plans on the host and enqueues one
+ *                                               copy of the forward and backward
+ *                                               metadata into ws on stream
+ *   pp_attn_fwd_planned(pl, ...) / pp_attn_bwd_planned(pl, ...)
+ *                                               enqueue kernels only, any number
+ *                                               of times (e.g. once per layer)
+ *   pp_plan_destroy(pl)                         frees the host record
+ *
+ * The planned calls compute exactly what pp_attn_fwd / pp_attn_bwd (or, with a
+ * rope_base, pp_attn_fwd_rope / pp_attn_bwd_rope) compute for the same pack and
+ * arguments.  Ownership: the plan (host memory, freed by pp_plan_destroy) refers
+ * to ws, which stays the caller's; ws must outlive the plan and must not be
+ * written by anything else while the plan is in use.  The planned calls also
+ * use ws as scratch (delta, fp32 casts), so calls on one plan must be ordered
+ * on one stream, after the stream that pp_plan_create used (or synchronised
+ * with it).  pp_plan_create copies the descriptor: the caller may free or
+ * change it afterwards.  A plan is bound to the dtype, head counts, head_dim and
+ * rope_base it was made with. */
+typedef struct pp_plan pp_plan;
+
+/* Workspace bytes of a plan for this pack and shape (forward and backward
+ * metadata and the backward's scratch).  Errors as pp_attn_fwd. */
+pp_status pp_plan_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                                 size_t* bytes);
+
+/* Builds a plan and enqueues its metadata copy into ws (dev, ws_bytes >=
+ * pp_plan_workspace_size's bytes) on hip_stream.  rope_base (host, may be NULL)
+ * selects the rotary variants.  *plan receives the handle, or NULL on error.
+ * Errors as pp_attn_fwd, plus PP_ERR_INVALID_ARGUMENT for a NULL plan pointer
+ * or a bad rope_base. */
+pp_status pp_plan_create(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                         const float* rope_base, void* ws, size_t ws_bytes, void* hip_stream, pp_plan** plan);
+
+/* Frees a plan's host record (NULL is accepted).  Does not touch ws. */
+pp_status pp_plan_destroy(pp_plan* plan);
+
+/* pp_attn_fwd (or pp_attn_fwd_rope when the plan has a rope_base; q_rot may be
+ * NULL, k_rot is required then and ignored otherwise) on a plan.  Tensor
+ * arguments, scale and errors as there; PP_ERR_INVALID_ARGUMENT for a NULL plan. */
+pp_status pp_attn_fwd_planned(const pp_plan* plan, float scale, const void* q, const void* k, const void* v,
+                              void* o, float* lse, void* q_rot, void* k_rot, void* hip_stream);
+
+/* pp_attn_bwd (or pp_attn_bwd_rope, with q, k the rotated ones) on a plan. */
+pp_status pp_attn_bwd_planned(const pp_plan* plan, float scale, const void* q, const void* k, const void* v,
+                              const void* o, const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                              void* hip_stream);
 
 /* Per-response sequence log-probabilities (Sec. 2.1 scores, Sec. 3.2 layout).
  * Token j of response k of row b sits at row-relative position t = o_bk + j; it

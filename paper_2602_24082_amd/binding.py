@@ -32,6 +32,7 @@ EXPORTED = [
     "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
     "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
+    "pp_plan_workspace_size", "pp_plan_create", "pp_plan_destroy", "pp_attn_fwd_planned", "pp_attn_bwd_planned",
 ]
 
 
@@ -88,6 +89,11 @@ def lib() -> ctypes.CDLL:
     L.pp_rope.argtypes = [D, i, i, i, f32, i, P, P, P, sz, P]
     L.pp_attn_fwd_rope.argtypes = [D, i, i, i, i, f32, f32, P, P, P, P, P, P, P, P, sz, P]
     L.pp_attn_bwd_rope.argtypes = [D, i, i, i, i, f32, f32, P, P, P, P, P, P, P, P, P, P, sz, P]
+    L.pp_plan_workspace_size.argtypes = [D, i, i, i, i, ctypes.POINTER(sz)]
+    L.pp_plan_create.argtypes = [D, i, i, i, i, ctypes.POINTER(f32), P, sz, P, ctypes.POINTER(P)]
+    L.pp_plan_destroy.argtypes = [P]
+    L.pp_attn_fwd_planned.argtypes = [P, f32, P, P, P, P, P, P, P, P]
+    L.pp_attn_bwd_planned.argtypes = [P, f32, P, P, P, P, P, P, P, P, P, P]
     L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_seq_logprob_bwd.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_rm_workspace_size.argtypes = [D, ctypes.POINTER(sz)]
@@ -265,6 +271,72 @@ def pp_attn_bwd_rope(pack: Pack, q_rot, k_rot, v, o, lse, dout, rope_base: float
     _check(lib().pp_attn_bwd_rope(h.ref, _dtype_code(q_rot), hq, hkv, d, float(scale), float(rope_base),
                                   _ptr(q_rot), _ptr(k_rot), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq),
                                   _ptr(dk), _ptr(dv), _ptr(ws), ws.numel(), _stream(q_rot.device)))
+    return dq, dk, dv
+
+
+class PlanHandle:
+    """A pp_plan handle and the workspace tensor it was staged into (kept alive
+    with it).  Free it with pp_plan_destroy (also done when it is collected)."""
+
+    def __init__(self, handle: ctypes.c_void_p, ws: torch.Tensor, hq: int, hkv: int, head_dim: int,
+                 rope_base: Optional[float]):
+        self.handle, self.ws = handle, ws
+        self.hq, self.hkv, self.head_dim, self.rope_base = hq, hkv, head_dim, rope_base
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.pp_plan_destroy(self.handle)
+            self.handle = None
+
+
+def pp_plan_workspace_size(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16) -> int:
+    h = _DescHolder(pack)
+    n = ctypes.c_size_t(0)
+    _check(lib().pp_plan_workspace_size(h.ref, dtype, hq, hkv, head_dim, ctypes.byref(n)))
+    return n.value
+
+
+def pp_plan_create(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16,
+                   rope_base: Optional[float] = None, ws: Optional[torch.Tensor] = None,
+                   device="cuda:0") -> PlanHandle:
+    """Plans the pack once and stages the metadata into ws on the current stream."""
+    h = _DescHolder(pack)
+    if ws is None:
+        ws = _workspace(pp_plan_workspace_size(pack, hq, hkv, head_dim, dtype), device)
+    base = ctypes.c_float(rope_base) if rope_base is not None else None
+    out = ctypes.c_void_p(None)
+    _check(lib().pp_plan_create(h.ref, dtype, hq, hkv, head_dim, ctypes.byref(base) if base is not None else None,
+                                _ptr(ws), ws.numel(), _stream(ws.device), ctypes.byref(out)))
+    return PlanHandle(out, ws, hq, hkv, head_dim, rope_base)
+
+
+def pp_plan_destroy(plan: PlanHandle):
+    if plan.handle:
+        _check(lib().pp_plan_destroy(plan.handle))
+        plan.handle = None
+
+
+def pp_attn_fwd_planned(plan: PlanHandle, q, k, v, scale: float = 0.0, out=None, lse=None, q_rot=None, k_rot=None):
+    """pp_attn_fwd (pp_attn_fwd_rope for a rotary plan) on a plan; returns
+    (o, lse) or, for a rotary plan, (o, lse, q_rot, k_rot)."""
+    T, hq, d = q.shape
+    out = torch.empty_like(q) if out is None else out
+    if lse is None:
+        lse = torch.empty(hq, T, dtype=torch.float32, device=q.device)
+    if plan.rope_base is not None and k_rot is None:
+        k_rot = torch.empty_like(k)
+    _check(lib().pp_attn_fwd_planned(plan.handle, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                     _ptr(q_rot), _ptr(k_rot), _stream(q.device)))
+    return (out, lse) if plan.rope_base is None else (out, lse, q_rot, k_rot)
+
+
+def pp_attn_bwd_planned(plan: PlanHandle, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, dk=None, dv=None):
+    """pp_attn_bwd (pp_attn_bwd_rope for a rotary plan, q and k rotated) on a plan."""
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    _check(lib().pp_attn_bwd_planned(plan.handle, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse),
+                                     _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _stream(q.device)))
     return dq, dk, dv
 
 

@@ -15,6 +15,7 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -788,42 +789,48 @@ struct RopeArgs {
 inline bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15) == 0; }
 inline bool aligned4(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 3) == 0; }
 
-pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
-                        const void* q, const void* k, const void* v, void* o, float* lse, const RopeArgs* rope,
-                        void* ws, size_t ws_bytes, void* hip_stream) {
-  Batch bt;
-  pp_status st = read_desc(desc, &bt);
-  if (st != PP_OK) return st;
-  if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
-  if ((st = check_dtype(dtype)) != PP_OK) return st;
-  if (rope && (st = check_rope_base(rope->base)) != PP_OK) return st;
-  if (bt.sumT > 0 && (!q || !k || !v || !o || !lse))
+pp_status check_fwd_ptrs(int sumT, const void* q, const void* k, const void* v, const void* o, const float* lse,
+                         const RopeArgs* rope) {
+  if (sumT > 0 && (!q || !k || !v || !o || !lse))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o and lse must be non-NULL");
-  if (bt.sumT > 0 && rope && !rope->k_rot) return fail(PP_ERR_INVALID_ARGUMENT, "k_rot must be non-NULL");
+  if (sumT > 0 && rope && !rope->k_rot) return fail(PP_ERR_INVALID_ARGUMENT, "k_rot must be non-NULL");
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned4(lse) ||
       (rope && (!aligned16(rope->k_rot) || !aligned16(rope->q_rot))))
     return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o (and q_rot, k_rot) must be 16-byte aligned, lse 4-byte aligned");
-  FwdPlan p;
-  plan_fwd(bt, dtype, hq, hkv, head_dim, &p);
-  if (ws_bytes < p.lay.total)
-    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "forward needs %zu workspace bytes, got %zu", p.lay.total,
-                ws_bytes);
-  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
-  if (bt.sumT == 0) return PP_OK;
-  hipStream_t s = (hipStream_t)hip_stream;
-  MetaImage img;
+  return PP_OK;
+}
+
+pp_status check_bwd_ptrs(int sumT, const void* q, const void* k, const void* v, const void* o, const float* lse,
+                         const void* dout, const void* dq, const void* dk, const void* dv) {
+  if (sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
+    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(dq) ||
+      !aligned16(dk) || !aligned16(dv) || !aligned4(lse))
+    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, dout, dq, dk and dv must be 16-byte aligned, lse 4-byte aligned");
+  return PP_OK;
+}
+
+// The forward's metadata prefix as one host image (rotary positions and
+// frequencies included when rope_base is given).
+void fwd_image(const Batch& bt, const FwdPlan& p, int head_dim, const double* rope_base, MetaImage* out) {
+  MetaImage& img = *out;
   img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
   img.put(p.lay.regions[p.r_items], p.q.items.data(), p.q.items.size() * sizeof(QTileItem));
   img.put(p.lay.regions[p.r_kt], p.q.ktiles.data(), p.q.ktiles.size() * sizeof(KTileEntry));
   std::vector<int32_t> pos;
   std::vector<double> freq;
-  if (rope) {
+  if (rope_base) {
     build_positions(bt, &pos);
-    build_inv_freq(head_dim, rope->base, &freq);
+    build_inv_freq(head_dim, *rope_base, &freq);
     img.put(p.lay.regions[p.r_pos], pos.data(), pos.size() * 4);
     img.put(p.lay.regions[p.r_freq], freq.data(), freq.size() * 8);
   }
-  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+}
+
+// Enqueues the forward on metadata already staged in ws.
+pp_status fwd_launch(const FwdPlan& p, void* ws, int sumT, pp_dtype dtype, int hq, int hkv, int head_dim,
+                     float scale, const void* q, const void* k, const void* v, void* o, float* lse,
+                     const RopeArgs* rope, hipStream_t s) {
   hipError_t e;
   const int32_t* d_pos = (const int32_t*)at(ws, p.lay, p.r_pos);
   const double* d_freq = (const double*)at(ws, p.lay, p.r_freq);
@@ -835,7 +842,7 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
     r.y = rope->k_rot;
     r.pos = d_pos;
     r.inv_freq = d_freq;
-    r.sumT = bt.sumT;
+    r.sumT = sumT;
     r.heads = hkv;
     r.head_dim = head_dim;
     r.inverse = false;
@@ -848,9 +855,9 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
     void* qb = at(ws, p.lay, p.cast.q);
     void* kb = at(ws, p.lay, p.cast.k);
     void* vb = at(ws, p.lay, p.cast.v);
-    if ((e = launch_to_bf16((const float*)q, qb, (int64_t)bt.sumT * hq * head_dim, s)) != hipSuccess ||
-        (e = launch_to_bf16((const float*)k, kb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess ||
-        (e = launch_to_bf16((const float*)v, vb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess)
+    if ((e = launch_to_bf16((const float*)q, qb, (int64_t)sumT * hq * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)k, kb, (int64_t)sumT * hkv * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)v, vb, (int64_t)sumT * hkv * head_dim, s)) != hipSuccess)
       return hip_fail(e, "fp32 to bf16 conversion launch");
     q = qb;
     k = kb;
@@ -869,7 +876,7 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   a.hq = hq;
   a.hkv = hkv;
   a.head_dim = head_dim;
-  a.sumT = bt.sumT;
+  a.sumT = sumT;
   a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
   a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
   if (rope) {
@@ -883,30 +890,35 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   return PP_OK;
 }
 
-pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
-                        const void* q, const void* k, const void* v, const void* o, const float* lse,
-                        const void* dout, void* dq, void* dk, void* dv, const float* rope_base, void* ws,
-                        size_t ws_bytes, void* hip_stream) {
+
+pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
+                        const void* q, const void* k, const void* v, void* o, float* lse, const RopeArgs* rope,
+                        void* ws, size_t ws_bytes, void* hip_stream) {
   Batch bt;
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
   if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
   if ((st = check_dtype(dtype)) != PP_OK) return st;
-  if (rope_base && (st = check_rope_base(*rope_base)) != PP_OK) return st;
-  if (bt.sumT > 0 && (!q || !k || !v || !o || !lse || !dout || !dq || !dk || !dv))
-    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, lse, dout, dq, dk and dv must be non-NULL");
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(dq) ||
-      !aligned16(dk) || !aligned16(dv) || !aligned4(lse))
-    return fail(PP_ERR_INVALID_ARGUMENT, "q, k, v, o, dout, dq, dk and dv must be 16-byte aligned, lse 4-byte aligned");
-  BwdPlan p;
-  plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
+  if (rope && (st = check_rope_base(rope->base)) != PP_OK) return st;
+  if ((st = check_fwd_ptrs(bt.sumT, q, k, v, o, lse, rope)) != PP_OK) return st;
+  FwdPlan p;
+  plan_fwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lay.total)
-    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", p.lay.total,
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "forward needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
   if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
   if (bt.sumT == 0) return PP_OK;
-  hipStream_t s = (hipStream_t)hip_stream;
   MetaImage img;
+  const double base = rope ? rope->base : 0.0;
+  fwd_image(bt, p, head_dim, rope ? &base : nullptr, &img);
+  hipStream_t s = (hipStream_t)hip_stream;
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  return fwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, rope, s);
+}
+
+// The backward's metadata prefix as one host image.
+void bwd_image(const Batch& bt, const BwdPlan& p, int head_dim, const double* rope_base, MetaImage* out) {
+  MetaImage& img = *out;
   img.put(p.lay.regions[p.r_seg], p.seg_lo.data(), p.seg_lo.size() * 4);
   img.put(p.lay.regions[p.r_seg_hi], p.seg_hi.data(), p.seg_hi.size() * 4);
   img.put(p.lay.regions[p.r_dq_items], p.dq.items.data(), p.dq.items.size() * sizeof(QTileItem));
@@ -920,7 +932,13 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
     img.put(p.lay.regions[p.r_pos], pos.data(), pos.size() * 4);
     img.put(p.lay.regions[p.r_freq], freq.data(), freq.size() * 8);
   }
-  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+}
+
+// Enqueues the backward on metadata already staged in ws.
+pp_status bwd_launch(const BwdPlan& p, void* ws, int sumT, pp_dtype dtype, int hq, int hkv, int head_dim,
+                     float scale, const void* q, const void* k, const void* v, const void* o,
+                     const float* lse, const void* dout, void* dq, void* dk, void* dv, bool rope,
+                     hipStream_t s) {
   hipError_t e;
   const void* dout_bf = dout;
   if (p.cast.on) {
@@ -928,10 +946,10 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
     void* kb = at(ws, p.lay, p.cast.k);
     void* vb = at(ws, p.lay, p.cast.v);
     void* db = at(ws, p.lay, p.cast.dout);
-    if ((e = launch_to_bf16((const float*)q, qb, (int64_t)bt.sumT * hq * head_dim, s)) != hipSuccess ||
-        (e = launch_to_bf16((const float*)k, kb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess ||
-        (e = launch_to_bf16((const float*)v, vb, (int64_t)bt.sumT * hkv * head_dim, s)) != hipSuccess ||
-        (e = launch_to_bf16((const float*)dout, db, (int64_t)bt.sumT * hq * head_dim, s)) != hipSuccess)
+    if ((e = launch_to_bf16((const float*)q, qb, (int64_t)sumT * hq * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)k, kb, (int64_t)sumT * hkv * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)v, vb, (int64_t)sumT * hkv * head_dim, s)) != hipSuccess ||
+        (e = launch_to_bf16((const float*)dout, db, (int64_t)sumT * hq * head_dim, s)) != hipSuccess)
       return hip_fail(e, "fp32 to bf16 conversion launch");
     q = qb;
     k = kb;
@@ -961,10 +979,10 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   a.hq = hq;
   a.hkv = hkv;
   a.head_dim = head_dim;
-  a.sumT = bt.sumT;
+  a.sumT = sumT;
   a.scale = scale > 0.f ? scale : 1.0f / std::sqrt((float)head_dim);
   a.dtype = dtype == PP_FP32 ? kFP32 : kBF16;
-  if (rope_base) {
+  if (rope) {
     a.rope = true;
     a.pos = (const int32_t*)at(ws, p.lay, p.r_pos);
     a.inv_freq = (const double*)at(ws, p.lay, p.r_freq);
@@ -972,6 +990,34 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   e = launch_attn_bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention backward launch");
   return PP_OK;
+}
+
+
+pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim, float scale,
+                        const void* q, const void* k, const void* v, const void* o, const float* lse,
+                        const void* dout, void* dq, void* dk, void* dv, const float* rope_base, void* ws,
+                        size_t ws_bytes, void* hip_stream) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (rope_base && (st = check_rope_base(*rope_base)) != PP_OK) return st;
+  if ((st = check_bwd_ptrs(bt.sumT, q, k, v, o, lse, dout, dq, dk, dv)) != PP_OK) return st;
+  BwdPlan p;
+  plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
+  if (ws_bytes < p.lay.total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", p.lay.total,
+                ws_bytes);
+  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (bt.sumT == 0) return PP_OK;
+  MetaImage img;
+  const double base = rope_base ? *rope_base : 0.0;
+  bwd_image(bt, p, head_dim, rope_base ? &base : nullptr, &img);
+  hipStream_t s = (hipStream_t)hip_stream;
+  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
+  return bwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, dout, dq, dk, dv,
+                    rope_base != nullptr, s);
 }
 
 // Workspace of pp_rope: positions then frequencies.
@@ -996,7 +1042,120 @@ pp_status check_rope_dim(int d) {
 }  // namespace
 }  // namespace pp
 
+// A staged attention plan: the pack's forward and backward metadata (work
+// lists, segment bounds, rotary positions) already in the caller's workspace,
+// with the host-side launch summary.  Built once per pack (Sec. 3.2's packing
+// is fixed for a training step) and reused by every layer's forward and
+// backward, which then enqueue kernels only.
+struct pp_plan {
+  pp_dtype dtype;
+  int hq, hkv, head_dim;
+  bool rope;
+  int sumT;
+  pp::FwdPlan fwd;
+  pp::BwdPlan bwd;
+  void* ws;        // caller's workspace: forward region first, backward at bwd_off
+  size_t bwd_off;
+};
+
+namespace pp {
+namespace {
+
+pp_status plan_common(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                      const float* rope_base, Batch* bt, pp_plan* p) {
+  pp_status st = read_desc(desc, bt);
+  if (st != PP_OK) return st;
+  if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_dtype(dtype)) != PP_OK) return st;
+  if (rope_base && (st = check_rope_base(*rope_base)) != PP_OK) return st;
+  p->dtype = dtype;
+  p->hq = hq;
+  p->hkv = hkv;
+  p->head_dim = head_dim;
+  p->rope = rope_base != nullptr;
+  p->sumT = bt->sumT;
+  plan_fwd(*bt, dtype, hq, hkv, head_dim, &p->fwd);
+  plan_bwd(*bt, dtype, hq, hkv, head_dim, &p->bwd);
+  p->bwd_off = align_up(p->fwd.lay.total);
+  return PP_OK;
+}
+
+}  // namespace
+}  // namespace pp
+
 extern "C" {
+
+pp_status pp_plan_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                                 size_t* bytes) {
+  if (!bytes) return fail(PP_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  Batch bt;
+  pp_plan p{};
+  pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, nullptr, &bt, &p);
+  if (st != PP_OK) return st;
+  *bytes = p.bwd_off + p.bwd.lay.total;
+  return PP_OK;
+}
+
+pp_status pp_plan_create(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                         const float* rope_base, void* ws, size_t ws_bytes, void* hip_stream, pp_plan** plan) {
+  if (!plan) return fail(PP_ERR_INVALID_ARGUMENT, "plan is NULL");
+  *plan = nullptr;
+  pp_plan* p = new (std::nothrow) pp_plan();
+  if (!p) return fail(PP_ERR_INVALID_ARGUMENT, "out of host memory for the plan");
+  Batch bt;
+  pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, rope_base, &bt, p);
+  const size_t total = p->bwd_off + p->bwd.lay.total;
+  if (st == PP_OK && ws_bytes < total)
+    st = fail(PP_ERR_WORKSPACE_TOO_SMALL, "the plan needs %zu workspace bytes, got %zu", total, ws_bytes);
+  if (st == PP_OK && total && !ws) st = fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (st == PP_OK && bt.sumT > 0) {
+    // one image: the forward's metadata at 0, the backward's at bwd_off
+    const double base = rope_base ? *rope_base : 0.0;
+    MetaImage fi, bi;
+    fwd_image(bt, p->fwd, head_dim, rope_base ? &base : nullptr, &fi);
+    bwd_image(bt, p->bwd, head_dim, rope_base ? &base : nullptr, &bi);
+    std::vector<uint8_t> img(p->bwd_off + bi.buf.size(), 0);
+    if (!fi.buf.empty()) memcpy(img.data(), fi.buf.data(), fi.buf.size());
+    if (!bi.buf.empty()) memcpy(img.data() + p->bwd_off, bi.buf.data(), bi.buf.size());
+    st = stage_copy(ws, img.data(), img.size(), (hipStream_t)hip_stream);
+  }
+  if (st != PP_OK) {
+    delete p;
+    return st;
+  }
+  p->ws = ws;
+  *plan = p;
+  return PP_OK;
+}
+
+pp_status pp_plan_destroy(pp_plan* plan) {
+  delete plan;
+  return PP_OK;
+}
+
+pp_status pp_attn_fwd_planned(const pp_plan* plan, float scale, const void* q, const void* k, const void* v,
+                              void* o, float* lse, void* q_rot, void* k_rot, void* hip_stream) {
+  if (!plan) return fail(PP_ERR_INVALID_ARGUMENT, "plan is NULL");
+  RopeArgs r{0.f, q_rot, k_rot};
+  const RopeArgs* rope = plan->rope ? &r : nullptr;
+  pp_status st = check_fwd_ptrs(plan->sumT, q, k, v, o, lse, rope);
+  if (st != PP_OK) return st;
+  if (plan->sumT == 0) return PP_OK;
+  return fwd_launch(plan->fwd, plan->ws, plan->sumT, plan->dtype, plan->hq, plan->hkv, plan->head_dim, scale, q, k,
+                    v, o, lse, rope, (hipStream_t)hip_stream);
+}
+
+pp_status pp_attn_bwd_planned(const pp_plan* plan, float scale, const void* q, const void* k, const void* v,
+                              const void* o, const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                              void* hip_stream) {
+  if (!plan) return fail(PP_ERR_INVALID_ARGUMENT, "plan is NULL");
+  pp_status st = check_bwd_ptrs(plan->sumT, q, k, v, o, lse, dout, dq, dk, dv);
+  if (st != PP_OK) return st;
+  if (plan->sumT == 0) return PP_OK;
+  void* ws_b = static_cast<char*>(plan->ws) + plan->bwd_off;
+  return bwd_launch(plan->bwd, ws_b, plan->sumT, plan->dtype, plan->hq, plan->hkv, plan->head_dim, scale, q, k, v, o,
+                    lse, dout, dq, dk, dv, plan->rope, (hipStream_t)hip_stream);
+}
 
 pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                       float scale, const void* q, const void* k, const void* v, void* o,

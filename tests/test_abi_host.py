@@ -293,3 +293,40 @@ def test_misaligned_tensors_rejected():
     fwd_r = lambda qr=ok, kr=ok: L.pp_attn_fwd_rope(ctypes.byref(d), 0, 4, 2, 128, 0.0, 10000.0, ok, ok, ok, ok, ok,
                                                     qr, kr, ok, nb, None)
     assert fwd_r(qr=off8) == 1 and fwd_r(kr=off8) == 1
+
+
+def test_plan_argument_checks():
+    """Reusable plans: size query, creation and the planned calls validate their
+    arguments on the host; a plan of an empty pack needs no copy, so its whole
+    lifecycle runs here."""
+    L = binding.lib()
+    ok = ctypes.c_void_p(4096)
+    d, keep = _raw_desc([0, 12], [4], [2], [4, 7], [3, 3], 2)
+    n = ctypes.c_size_t(0)
+    assert L.pp_plan_workspace_size(ctypes.byref(d), 0, 4, 2, 128, ctypes.byref(n)) == 0
+    f, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert L.pp_workspace_size(ctypes.byref(d), 0, 4, 2, 128, 0, ctypes.byref(f), ctypes.byref(b), None, None) == 0
+    assert n.value >= f.value + b.value
+    assert L.pp_plan_workspace_size(ctypes.byref(d), 0, 4, 2, 96, ctypes.byref(n)) == 3
+    assert L.pp_plan_workspace_size(ctypes.byref(d), 0, 4, 3, 128, ctypes.byref(n)) == 1
+    assert L.pp_plan_workspace_size(ctypes.byref(d), 0, 4, 2, 128, None) == 1
+    h = ctypes.c_void_p(1234)
+    assert L.pp_plan_create(ctypes.byref(d), 0, 4, 2, 128, None, ok, 1 << 30, None, None) == 1
+    assert L.pp_plan_create(ctypes.byref(d), 0, 4, 2, 128, None, ok, 16, None, ctypes.byref(h)) == 4
+    assert h.value is None  # no handle on error
+    bad = ctypes.c_float(-1.0)
+    assert L.pp_plan_create(ctypes.byref(d), 0, 4, 2, 128, ctypes.byref(bad), ok, 1 << 30, None,
+                            ctypes.byref(h)) == 1
+    assert L.pp_attn_fwd_planned(None, 0.0, ok, ok, ok, ok, ok, None, None, None) == 1
+    assert L.pp_attn_bwd_planned(None, 0.0, ok, ok, ok, ok, ok, ok, ok, ok, ok, None) == 1
+    assert L.pp_plan_destroy(None) == 0
+    # an empty pack (one row of no tokens): create, use and destroy without a device
+    e, keep_e = _raw_desc([0, 0], [0], [0], [0], [0], 1)
+    assert L.pp_plan_workspace_size(ctypes.byref(e), 0, 4, 2, 128, ctypes.byref(n)) == 0
+    ws = ctypes.c_void_p(4096) if n.value else None
+    assert L.pp_plan_create(ctypes.byref(e), 0, 4, 2, 128, None, ws, n.value, None, ctypes.byref(h)) == 0
+    assert h.value is not None
+    assert L.pp_attn_fwd_planned(h, 0.0, ok, ok, ok, ok, ok, None, None, None) == 0
+    assert L.pp_attn_fwd_planned(h, 0.0, ok, ok, ctypes.c_void_p(4096 + 8), ok, ok, None, None, None) == 1
+    assert L.pp_attn_bwd_planned(h, 0.0, ok, ok, ok, ok, ok, ok, ok, ok, ok, None) == 0
+    assert L.pp_plan_destroy(h) == 0

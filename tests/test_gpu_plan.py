@@ -1,0 +1,101 @@
+"""GPU tests of the reusable plan (pp_plan_create + pp_attn_{fwd,bwd}_planned).
+
+The planned calls run the same kernels on the same metadata as the
+self-contained entry points, so their outputs must be bit-identical to
+pp_attn_fwd / pp_attn_bwd (and the rotary variants) for the same inputs; one
+case is also checked against the oracle directly, at the attention tolerances
+(O, LSE max-abs <= 1e-2; dQ, dK, dV relative Frobenius <= 2e-2).  A plan is
+reused for several "layers" (different q, k, v) and does not depend on the
+caller's descriptor arrays after creation.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import pp_oracle as orc
+from paper_2602_24082_amd import binding as pp
+from paper_2602_24082_amd import workload as wl
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _ragged():
+    return wl.make_pack([300, 0, 129, 5, 64], [[70, 45], [33, 64], [1, 0, 200], [130], [64, 64]],
+                        pad=[3, 0, 0, 17, 0])
+
+
+@pytest.mark.parametrize("dtype,d,hq,hkv", [(torch.bfloat16, 128, 8, 2), (torch.bfloat16, 64, 4, 4),
+                                            (torch.float32, 64, 4, 2)])
+def test_planned_equals_self_contained(dtype, d, hq, hkv):
+    pack = _ragged()
+    print(f"case plan T={pack.total_tokens} d={d} hq={hq} hkv={hkv} {dtype}", flush=True)
+    code = pp.PP_FP32 if dtype == torch.float32 else pp.PP_BF16
+    plan = pp.pp_plan_create(pack, hq, hkv, d, dtype=code, device=DEV)
+    for layer in range(3):
+        q, k, v, do = wl.qkv(pack, hq, hkv, d, 300 + layer, dtype, device=DEV)
+        o1, l1 = pp.pp_attn_fwd(pack, q, k, v)
+        o2, l2 = pp.pp_attn_fwd_planned(plan, q, k, v)
+        g1 = pp.pp_attn_bwd(pack, q, k, v, o1, l1, do)
+        g2 = pp.pp_attn_bwd_planned(plan, q, k, v, o2, l2, do)
+        torch.cuda.synchronize()
+        assert torch.equal(o1, o2) and torch.equal(l1, l2), layer
+        for a, b in zip(g1, g2):
+            assert torch.equal(a, b), layer
+    pp.pp_plan_destroy(plan)
+
+
+def test_planned_matches_oracle():
+    pack = _ragged()
+    hq, hkv, d = 8, 2, 128
+    print(f"case plan-oracle T={pack.total_tokens}", flush=True)
+    # the binding's descriptor arrays are released as soon as pp_plan_create
+    # returns: the plan keeps its own copy of everything it needs
+    plan = pp.pp_plan_create(pack, hq, hkv, d, device=DEV)
+    q, k, v, do = wl.qkv(pack, hq, hkv, d, 41, torch.bfloat16, device="cpu")
+    o, lse = pp.pp_attn_fwd_planned(plan, *(x.to(DEV) for x in (q, k, v)))
+    dq, dk, dv = pp.pp_attn_bwd_planned(plan, q.to(DEV), k.to(DEV), v.to(DEV), o, lse, do.to(DEV))
+    args = pack.oracle_args()
+    qn, kn, vn, don = (x.double().numpy() for x in (q, k, v, do))
+    O, L = orc.attn_fwd(*args, qn, kn, vn)
+    assert np.abs(o.double().cpu().numpy() - O).max() <= 1e-2
+    assert np.abs(lse.double().cpu().numpy() - L).max() <= 1e-2
+    for got, ref in zip((dq, dk, dv), orc.attn_bwd(*args, qn, kn, vn, don)):
+        g = got.double().cpu().numpy()
+        assert np.isfinite(g).all()
+        assert np.linalg.norm(g - ref) / np.linalg.norm(ref) <= 2e-2
+
+
+def test_rotary_plan_equals_rotary_entry_points():
+    pack = wl.make_pack([500, 77], [[100, 28, 300], [64, 64]], pad=[0, 5])
+    hq, hkv, d, base = 8, 2, 128, 500000.0
+    print(f"case plan-rope T={pack.total_tokens}", flush=True)
+    q, k, v, do = wl.qkv(pack, hq, hkv, d, 77, torch.bfloat16, device=DEV)
+    plan = pp.pp_plan_create(pack, hq, hkv, d, rope_base=base, device=DEV)
+    o1, l1, qr1, kr1 = pp.pp_attn_fwd_rope(pack, q, k, v, base)
+    qr2 = torch.empty_like(q)
+    o2, l2, qr2, kr2 = pp.pp_attn_fwd_planned(plan, q, k, v, q_rot=qr2)
+    g1 = pp.pp_attn_bwd_rope(pack, qr1, kr1, v, o1, l1, do, base)
+    g2 = pp.pp_attn_bwd_planned(plan, qr2, kr2, v, o2, l2, do)
+    torch.cuda.synchronize()
+    for a, b in [(o1, o2), (l1, l2), (qr1, qr2), (kr1, kr2), *zip(g1, g2)]:
+        assert torch.equal(a, b)
+    pp.pp_plan_destroy(plan)
+
+
+def test_planned_full_size_workload_matches_self_contained():
+    """The 8B-shaped benchmark batch: planned == self-contained, bit for bit."""
+    cfg = wl.CONFIGS[1]
+    pack = wl.config_pack(cfg)
+    print(f"case plan-fullsize {cfg.name} T={pack.total_tokens}", flush=True)
+    q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, 9, torch.bfloat16, DEV)
+    plan = pp.pp_plan_create(pack, cfg.hq, cfg.hkv, cfg.head_dim, device=DEV)
+    o1, l1 = pp.pp_attn_fwd(pack, q, k, v)
+    o2, l2 = pp.pp_attn_fwd_planned(plan, q, k, v)
+    g1 = pp.pp_attn_bwd(pack, q, k, v, o1, l1, do)
+    g2 = pp.pp_attn_bwd_planned(plan, q, k, v, o2, l2, do)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
