@@ -43,10 +43,10 @@ def _poisoned_like(t):
     return torch.full_like(t, float("nan"))
 
 
-def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True):
+def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None, grads=("dq", "dk", "dv")):
     print(f"case rows={pack.num_rows} T={pack.total_tokens} hq={hq} hkv={hkv} d={d} {dtype} seed={seed}",
           flush=True)
-    q, k, v, do = _inputs(pack, hq, hkv, d, dtype, seed)
+    q, k, v, do = _inputs(pack, hq, hkv, d, dtype, seed) if inputs is None else inputs
     qg, kg, vg, dog = (x.to(DEV) for x in (q, k, v, do))
     T = pack.total_tokens
     o = _poisoned_like(qg)
@@ -68,8 +68,9 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True):
     for name, got, ref in (("dq", dq, dq_r), ("dk", dk, dk_r), ("dv", dv, dv_r)):
         g = got.double().cpu().numpy()
         assert np.isfinite(g).all(), f"unwritten {name}"
-        err = _rel_fro(g, ref)
-        assert err <= G_TOL, (name, err)
+        if name in grads:
+            err = _rel_fro(g, ref)
+            assert err <= G_TOL, (name, err)
     # padding rows are exactly zero
     seg = orc.pack_segment_ids(*args)
     pad = seg < 0
@@ -108,6 +109,50 @@ def test_edge_cases():
     _check_attention(pack, 4, 1, 64, torch.bfloat16, 41)
     pack = wl.make_pack([5, 0], [[], []], pad=[0, 9])  # all-padding second row
     _check_attention(pack, 2, 2, 128, torch.bfloat16, 42)
+
+
+def test_large_scores():
+    """Scores with standard deviation 16 (q, k ~ N(0, 2) per element, d = 128):
+    nearly one-hot softmax rows whose maximum jumps between key tiles, so the
+    forward's lazily raised reference maximum is raised often.  V is halved so
+    that the bf16 rounding of one dominant P (2^-9 relative) stays inside the
+    1e-2 bound on O."""
+    pack = wl.make_pack([300, 90], [[70, 45], [33, 64, 10]], pad=[3, 0])
+    hq, hkv, d = 4, 2, 128
+    q, k, v, do = _inputs(pack, hq, hkv, d, torch.bfloat16, 61)
+    q = (q.float() * 2).to(torch.bfloat16)
+    k = (k.float() * 2).to(torch.bfloat16)
+    v = (v.float() * 0.5).to(torch.bfloat16)
+    _check_attention(pack, hq, hkv, d, torch.bfloat16, 61, inputs=(q, k, v, do))
+
+
+def test_scores_rising_along_the_row():
+    """Every query's score grows by 0.2 per key position (plus small noise), so
+    the running maximum rises by more than the rescale slack on every key tile
+    and the softmax mass sits on each query's latest visible keys: the rescale
+    branch runs on nearly every tile of the forward.  O, LSE, dV and dK are
+    checked.  dQ is not: here dQ_i = scale sum_j dS_ij k_j sums near-one-hot
+    dS_ij (whose row sums are exactly 0) against keys that share one component
+    of size up to ~1000, so the bf16 rounding of dS (2^-9 relative per element,
+    as in any bf16 flash backward) is amplified by that component over its
+    spread inside the softmax window -- an ill-conditioned sum the gradient
+    tolerance does not cover.  dQ is checked by every other case."""
+    pack = wl.make_pack([300, 200], [[100, 130], [64, 97, 40]], pad=[0, 7])
+    hq, hkv, d = 4, 2, 128
+    q, k, v, do = _inputs(pack, hq, hkv, d, torch.bfloat16, 62)
+    T = pack.total_tokens
+    pos = torch.zeros(T)
+    rs = np.asarray(pack.row_start)
+    for b in range(pack.num_rows):
+        pos[rs[b]:rs[b + 1]] = torch.arange(rs[b + 1] - rs[b], dtype=torch.float32)
+    scale = 1.0 / math.sqrt(d)
+    qf = q.float() * 0.05
+    kf = k.float() * 0.05
+    qf[:, :, 0] = 1.0
+    kf[:, :, 0] = (0.2 / scale) * pos[:, None]
+    q, k = qf.to(torch.bfloat16), kf.to(torch.bfloat16)
+    v = (v.float() * 0.5).to(torch.bfloat16)
+    _check_attention(pack, hq, hkv, d, torch.bfloat16, 62, inputs=(q, k, v, do), grads=("dk", "dv"))
 
 
 def test_g8_long_prefix_small():
