@@ -28,8 +28,17 @@
 namespace pp {
 namespace {
 
-constexpr int kLpThreads = 256;
-constexpr int kLpUnroll = 4;  // 16-byte vectors in flight per thread per step
+// threads per log-prob workgroup (one workgroup per logit row: 1024 threads
+// with 4 vectors each keep 64 KB of the row in flight) and 16-byte vectors in
+// flight per thread
+#ifndef PP_LP_THREADS
+#define PP_LP_THREADS 1024
+#endif
+#ifndef PP_LP_UNROLL
+#define PP_LP_UNROLL 4
+#endif
+constexpr int kLpThreads = PP_LP_THREADS;
+constexpr int kLpUnroll = PP_LP_UNROLL;  // 16-byte vectors in flight per thread per step
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
