@@ -302,17 +302,27 @@ __global__ __launch_bounds__(kLpThreads) void logprob_bwd_kernel(LogprobBwdLaunc
   }
 }
 
-// Log-prob backward with the row held in registers: one 512-thread workgroup
+// Log-prob backward with the row held in registers: one 1024-thread workgroup
 // per flat logit row.  A needed row is read from HBM once -- thread t loads the
-// 16-byte vectors t, t + 512, ... (up to kLpbVecs of them) -- its logsumexp is
+// 16-byte vectors t, t + 1024, ... (up to kLpbVecs of them) -- its logsumexp is
 // formed from the registers (thread maximum, then thread sum of exponentials,
 // then a fixed-order workgroup combine), and the gradient is computed from the
 // same registers and streamed out, so each row costs one read and one write of
 // HBM (the two-pass kernel above reads it twice).  Rows that predict nothing
 // are streamed zeros.  Used when the row's 16-byte vectors fit
-// (vocab <= 512 * kLpbVecs * elements per vector) and rows are 16-byte aligned.
-constexpr int kLpbThreads = 512;
-constexpr int kLpbVecs = 40;
+// (vocab <= kLpbThreads * kLpbVecs * elements per vector: 131072 bf16 or 65536
+// fp32 values) and rows are 16-byte aligned.  1024 threads x 16 vectors holds a
+// 128256-entry bf16 row in 111 VGPRs without spilling; at 4 waves per SIMD it
+// kept HBM busier than 512 x 40 (2 waves per SIMD, 0.73 against 0.77 ms on the
+// 8B-shaped batch) and than 768 x 27 or 1024 x 20 (both spill).
+#ifndef PP_LPB_THREADS
+#define PP_LPB_THREADS 1024
+#endif
+#ifndef PP_LPB_VECS
+#define PP_LPB_VECS 16
+#endif
+constexpr int kLpbThreads = PP_LPB_THREADS;
+constexpr int kLpbVecs = PP_LPB_VECS;
 
 template <int R>
 __device__ __forceinline__ void opaque(u32x4 (&u)[R]) {

@@ -76,6 +76,14 @@ def test_logprob_bwd_llama_vocab_k4():
     _check_bwd(pack, 128256, torch.bfloat16, 3.0, 175)
 
 
+def test_logprob_bwd_register_row_limit():
+    # fp32 rows of exactly 1024 threads x 16 vectors x 4 values (held in
+    # registers, read once) and one 16-byte vector longer (the two-read kernel)
+    pack = wl.make_pack([6, 3], [[5, 2], [4, 1, 3]], pad=[1, 0])
+    _check_bwd(pack, 65536, torch.float32, 3.0, 185)
+    _check_bwd(pack, 65540, torch.float32, 3.0, 186)
+
+
 def test_logprob_bwd_takes_the_loss_gradient():
     # the DPO chain: forward scores, loss gradient, then logits gradient
     pack = wl.make_pack([30, 12, 20], [[10, 14], [7, 9], [5, 6]])
