@@ -305,43 +305,14 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     }
     const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
     const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
-    // dV^T += dO^T P and dK^T += Q^T dS: product n is block m = n / 4 of dV (n
-    // even) or dK (n odd) over query rows 0-15 (n % 4 < 2) or 16-31 of the
-    // half; the transposed fragments are read PD products ahead (PD 0: each
-    // right before its MFMA, the compiler's schedule)
-    {
-      constexpr int NI = 4 * (D / 32), PD = PP_DKDV_TR_PREFETCH;
-      auto frag = [&](int n) {
-        return lds_tr8<D>((n & 1) ? sg.q : sg.dout, qb * 32 + 16 * ((n >> 1) & 1), 32 * (n >> 2), lane);
-      };
-      if constexpr (PD == 0) {
+    // dV^T += dO^T P and dK^T += Q^T dS over the half's two 16-query chunks,
+    // each transposed fragment read right before its MFMA
 #pragma unroll
-        for (int m = 0; m < D / 32; ++m) {
-          acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
-          acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32, 32 * m, lane), db0, acc_dk[m]);
-          acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
-          acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
-        }
-      } else {
-      bf16x8 a[PD + 1];
-#pragma unroll
-      for (int n = 0; n < PD; ++n) a[n] = frag(n);
-#pragma unroll
-      for (int n = 0; n < NI; ++n) {
-        if (n + PD < NI) a[(n + PD) % (PD + 1)] = frag(n + PD);
-        const int m = n >> 2, t = n & 3;
-        const bf16x8& b = t == 0 ? pb0 : t == 1 ? db0 : t == 2 ? pb1 : db1;
-        if (t & 1) acc_dk[m] = mfma32(a[n % (PD + 1)], b, acc_dk[m]);
-        else acc_dv[m] = mfma32(a[n % (PD + 1)], b, acc_dv[m]);
-      }
-#pragma unroll
-      for (int n = 0; n < PD; ++n) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
-#pragma unroll
-      for (int n = 0; n < NI; ++n) {
-        if (n + PD < NI) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-      }
-      }
+    for (int m = 0; m < D / 32; ++m) {
+      acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32, 32 * m, lane), pb0, acc_dv[m]);
+      acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32, 32 * m, lane), db0, acc_dk[m]);
+      acc_dv[m] = mfma32(lds_tr8<D>(sg.dout, qb * 32 + 16, 32 * m, lane), pb1, acc_dv[m]);
+      acc_dk[m] = mfma32(lds_tr8<D>(sg.q, qb * 32 + 16, 32 * m, lane), db1, acc_dk[m]);
     }
   }
 
@@ -515,35 +486,12 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
       db[2 * kb] = acc_half_to_bf16(dp[kb], 0);
       db[2 * kb + 1] = acc_half_to_bf16(dp[kb], 1);
     }
-    // dQ^T += K^T dS^T: product n is block m = n % (D/32) over keys 16 ch ..
-    // +15, ch = n / (D/32); the transposed K fragments are read PD ahead (PD 0:
-    // each right before its MFMA)
-    {
-      constexpr int NM = D / 32, NI = 2 * QKB * NM, PD = PP_DQ_TR_PREFETCH;
-      auto frag = [&](int n) { return lds_tr8<D>(sK, 16 * (n / NM), 32 * (n % NM), lane); };
-      if constexpr (PD == 0) {
+    // dQ^T += K^T dS^T over 16-key chunks, each transposed K fragment read
+    // right before its MFMA
 #pragma unroll
-        for (int ch = 0; ch < 2 * QKB; ++ch)
+    for (int ch = 0; ch < 2 * QKB; ++ch)
 #pragma unroll
-          for (int m = 0; m < NM; ++m) acc[m] = mfma32(lds_tr8<D>(sK, 16 * ch, 32 * m, lane), db[ch], acc[m]);
-      } else {
-      bf16x8 a[PD + 1];
-#pragma unroll
-      for (int n = 0; n < PD; ++n) a[n] = frag(n);
-#pragma unroll
-      for (int n = 0; n < NI; ++n) {
-        if (n + PD < NI) a[(n + PD) % (PD + 1)] = frag(n + PD);
-        acc[n % NM] = mfma32(a[n % (PD + 1)], db[n / NM], acc[n % NM]);
-      }
-#pragma unroll
-      for (int n = 0; n < PD; ++n) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
-#pragma unroll
-      for (int n = 0; n < NI; ++n) {
-        if (n + PD < NI) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-      }
-      }
-    }
+      for (int m = 0; m < D / 32; ++m) acc[m] = mfma32(lds_tr8<D>(sK, 16 * ch, 32 * m, lane), db[ch], acc[m]);
   }
 
   if (!in_tile) return;

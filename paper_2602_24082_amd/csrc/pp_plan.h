@@ -52,14 +52,6 @@ namespace pp {
 #ifndef PP_DQ_PREFETCH
 #define PP_DQ_PREFETCH 3
 #endif
-// transposed fragments the backward kernels read ahead of the MFMA that
-// consumes them (dV / dK and dQ products)
-#ifndef PP_DKDV_TR_PREFETCH
-#define PP_DKDV_TR_PREFETCH 0
-#endif
-#ifndef PP_DQ_TR_PREFETCH
-#define PP_DQ_TR_PREFETCH 0
-#endif
 
 // Tile sizes of the kernels (rows of the flat token axis).  Each wave of the
 // forward and dQ kernels owns 32 queries; each wave of the dK/dV kernel owns
