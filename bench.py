@@ -464,31 +464,11 @@ def main():
             pp.pp_seq_logprob(pack, logits_ref, tokens, seq=seq_ref, ws=ws_lp)
         return pp.pp_dpo_loss(num_resp, seq_pol, seq_ref if with_ref else None, beta, ws=ws_loss)
 
-    for _ in range(args.warmup):
-        step(False)
-    torch.cuda.synchronize()
-    pp.pp_timing_reset()
-    pp.pp_timing_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        loss, _, _ = step(True)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    pp.pp_timing_enable(False)
-    kern = pp.pp_timing_get()
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    attn_each = [a.elapsed_time(b) for a, b in attn_ev]
-    attn_ms = sum(attn_each) / args.steps
-    loss_val = float(loss.item())
-
     U = useful_pairs(pack)
     d, hq = cfg.head_dim, cfg.hq
     fwd_flops = 4 * d * hq * U
     bwd_flops = 10 * d * hq * U
     useful = fwd_flops + bwd_flops
-    tflops = useful / (attn_ms * 1e-3) / 1e12
-
     # algorithmic work per launch of each kernel (FLOPs of the GEMMs its algorithm
     # performs, or bytes it must move)
     n_rows = logit_rows_needed(pack)
@@ -498,7 +478,41 @@ def main():
         "pp_attn_bwd_dq": ("mfma", 6 * d * hq * U),
         "pp_logprob_rows": ("hbm", n_rows * V * 2 + n_rows * 16),
     }
-    dom = max((k for k in kern if k in per_launch), key=lambda k: kern[k][0])
+
+    for _ in range(args.warmup):
+        step(False)
+    # per-kernel breakdown: a short pass with every launch between hipEvents picks
+    # the kernel with the largest time per step; the timed steps then carry events
+    # on that kernel alone, so the rest of each step runs as it does untimed
+    torch.cuda.synchronize()
+    n_breakdown = max(3, min(args.steps, 10))
+    pp.pp_timing_select(None)
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    for _ in range(n_breakdown):
+        step(False)
+    torch.cuda.synchronize()
+    pp.pp_timing_enable(False)
+    kern_all = pp.pp_timing_get()
+    dom = max((k for k in kern_all if k in per_launch), key=lambda k: kern_all[k][0])
+    pp.pp_timing_select([dom])
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        loss, _, _ = step(True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pp.pp_timing_enable(False)
+    pp.pp_timing_select(None)
+    kern = pp.pp_timing_get()  # the dominant kernel, over the timed steps
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    attn_each = [a.elapsed_time(b) for a, b in attn_ev]
+    attn_ms = sum(attn_each) / args.steps
+    loss_val = float(loss.item())
+    tflops = useful / (attn_ms * 1e-3) / 1e12
+
     bound, work = per_launch[dom]
     avg_ms = kern[dom][0] / kern[dom][1]
     traffic = traffic_from_profile(dom) if args.config == 1 else None
@@ -512,16 +526,16 @@ def main():
         roof = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "algorithmic_bytes_per_launch": work, "avg_launch_ms": round(avg_ms, 4)}
-    kernels = {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in kern.items()}
+    kernels = {k: {"avg_ms": round(v[0] / v[1], 4), "launches": v[1]} for k, v in kern_all.items()}
     # every attention kernel against the bf16 MFMA peak (algorithmic FLOPs per launch)
     attn_roofs = {}
     for k in ("pp_attn_fwd", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq"):
-        if k in kern:
-            k_ms = kern[k][0] / kern[k][1]
+        if k in kern_all:
+            k_ms = kern_all[k][0] / kern_all[k][1]
             ach = per_launch[k][1] / (k_ms * 1e-3) / 1e12
             attn_roofs[k] = {"achieved_TFLOP_s": round(ach, 1), "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                              "avg_ms": round(k_ms, 4), "algorithmic_flops_per_launch": per_launch[k][1]}
-    lp = kern.get("pp_logprob_rows")
+    lp = kern.get("pp_logprob_rows") or kern_all.get("pp_logprob_rows")
     logprob = None
     if lp:
         lp_ms = lp[0] / lp[1]
@@ -622,6 +636,7 @@ def main():
         "rope": rope,
         "plan": plan,
         "kernels": kernels,
+        "kernel_breakdown_steps": n_breakdown,
         "attention_rooflines": attn_roofs,
         "roofline": roof,
         "cpu_baseline": cpu,

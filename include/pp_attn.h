@@ -360,6 +360,11 @@ pp_status pp_tile_class_len(const pp_pack_desc* desc, int block_q, int block_k, 
  * kernel's name (static string), its total elapsed milliseconds and its launch
  * count. */
 pp_status pp_timing_enable(int on);
+/* Restricts timing to the launches named in `names`, a comma-separated list of
+ * the names pp_timing_get reports (e.g. "pp_logprob_rows,pp_attn_fwd"); NULL or
+ * "" times every launch again.  The list is copied.  Launches left out get no
+ * events, so the work around them runs as it would untimed. */
+pp_status pp_timing_select(const char* names);
 pp_status pp_timing_reset(void);
 int pp_timing_count(void);
 pp_status pp_timing_get(int idx, const char** name, double* total_ms, int64_t* launches);

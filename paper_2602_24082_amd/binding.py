@@ -29,7 +29,7 @@ STATUS = {0: "PP_OK", 1: "PP_ERR_INVALID_ARGUMENT", 2: "PP_ERR_BAD_LAYOUT", 3: "
 EXPORTED = [
     "pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_seq_logprob_bwd", "pp_dpo_loss",
     "pp_rm_workspace_size", "pp_rm_scores", "pp_rm_scores_bwd", "pp_pack_stats",
-    "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
+    "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_select", "pp_timing_reset",
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
     "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
     "pp_plan_workspace_size", "pp_plan_create", "pp_plan_destroy", "pp_attn_fwd_planned", "pp_attn_bwd_planned",
@@ -104,6 +104,7 @@ def lib() -> ctypes.CDLL:
     L.pp_pack_export.argtypes = [D, i, i, P, P, P, sz]
     L.pp_tile_class_len.argtypes = [D, i, i, ctypes.POINTER(sz)]
     L.pp_timing_enable.argtypes = [i]
+    L.pp_timing_select.argtypes = [ctypes.c_char_p]
     L.pp_timing_reset.argtypes = []
     L.pp_timing_count.argtypes = []
     L.pp_timing_count.restype = i
@@ -115,8 +116,8 @@ def lib() -> ctypes.CDLL:
     L.pp_last_error.restype = ctypes.c_char_p
     L.pp_version.restype = i
     for name in ("pp_workspace_size", "pp_attn_fwd", "pp_attn_bwd", "pp_seq_logprob", "pp_dpo_loss",
-                 "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_reset",
-                 "pp_timing_get"):
+                 "pp_pack_export", "pp_tile_class_len", "pp_timing_enable", "pp_timing_select",
+                 "pp_timing_reset", "pp_timing_get"):
         getattr(L, name).restype = i
     _lib = L
     return L
@@ -467,6 +468,12 @@ def pp_pack_export(pack: Pack, block_q: int = 128, block_k: int = 64, tiles: boo
 
 def pp_timing_enable(on: bool = True):
     _check(lib().pp_timing_enable(1 if on else 0))
+
+
+def pp_timing_select(names=None):
+    """Time only the named launches (iterable of names, or None for all)."""
+    arg = None if not names else ",".join(names).encode()
+    _check(lib().pp_timing_select(arg))
 
 
 def pp_timing_reset():

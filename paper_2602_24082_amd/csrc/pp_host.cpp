@@ -14,6 +14,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <mutex>
 #include <new>
 #include <string>
@@ -418,36 +419,56 @@ struct Layout {
 // ---------------------------------------------------------------------------
 
 struct StagingSlot {
-  void* host = nullptr;
+  void* host = nullptr;       // mapped pinned host memory
+  void* dev = nullptr;        // its device address (null: copies go through hipMemcpyAsync)
   size_t cap = 0;
-  hipEvent_t done = nullptr;
+  hipEvent_t done = nullptr;  // recorded on the copy's stream (its device's event)
   bool pending = false;
 };
 
+// One ring per device: an event belongs to the device that was current when it
+// was created, and a mapped address to the device it was taken for, so slots
+// are never shared between devices.  A slot outgrown by a larger image is kept
+// (in `retired`) rather than freed: a kernel has read it, and pinned memory is
+// only released at unload.
+struct StagingRing {
+  StagingSlot slot[8];
+  int next = 0;
+  std::vector<void*> retired;
+};
+
 std::mutex g_stage_mu;
-StagingSlot g_stage[8];
-int g_stage_next = 0;
+std::map<int, StagingRing> g_stage;
 
 struct StagingRelease {
   ~StagingRelease() {
     // Only free what is no longer in flight; the runtime may already be down at
     // unload, in which case the OS reclaims the memory.
-    for (auto& s : g_stage) {
-      if (s.pending && s.done) hipEventSynchronize(s.done);
-      if (s.done) hipEventDestroy(s.done);
-      if (s.host) hipHostFree(s.host);
-      s = StagingSlot{};
+    for (auto& kv : g_stage) {
+      for (auto& s : kv.second.slot) {
+        if (s.pending && s.done) hipEventSynchronize(s.done);
+        if (s.done) hipEventDestroy(s.done);
+        if (s.host) hipHostFree(s.host);
+        s = StagingSlot{};
+      }
+      for (void* h : kv.second.retired) hipHostFree(h);
+      kv.second.retired.clear();
     }
   }
 } g_stage_release;
 
-// Copies `bytes` from `src` into device memory `dst` through a pinned slot.
+// Copies `bytes` from `src` into device memory `dst` (on the current device,
+// whose stream `stream` is) through a pinned slot of that device's ring: the
+// host fills the slot and a kernel on `stream` copies it into `dst`.
 pp_status stage_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
   if (bytes == 0) return PP_OK;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice(staging)");
   std::lock_guard<std::mutex> lk(g_stage_mu);
-  StagingSlot& s = g_stage[g_stage_next];
-  g_stage_next = (g_stage_next + 1) % 8;
-  hipError_t e;
+  StagingRing& ring = g_stage[dev];
+  StagingSlot& s = ring.slot[ring.next];
+  ring.next = (ring.next + 1) % 8;
   if (s.pending) {
     e = hipEventSynchronize(s.done);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(staging)");
@@ -458,17 +479,26 @@ pp_status stage_copy(void* dst, const void* src, size_t bytes, hipStream_t strea
     if (e != hipSuccess) return hip_fail(e, "hipEventCreate(staging)");
   }
   if (s.cap < bytes) {
-    if (s.host) hipHostFree(s.host);
-    s.host = nullptr;
+    if (s.host) ring.retired.push_back(s.host);
+    s.host = s.dev = nullptr;
     s.cap = 0;
     size_t cap = std::max<size_t>(bytes, 1 << 20);
-    e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+    // coherent: the copy kernel reads what the host just wrote, never a cached line
+    e = hipHostMalloc(&s.host, cap, hipHostMallocMapped | hipHostMallocCoherent);
     if (e != hipSuccess) return hip_fail(e, "hipHostMalloc(staging)");
     s.cap = cap;
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, s.host, 0) == hipSuccess) s.dev = d;
+    else (void)hipGetLastError();  // no mapped address: this slot copies with hipMemcpyAsync
   }
   memcpy(s.host, src, bytes);
-  e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(plan)");
+  if (s.dev && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+    e = launch_stage_copy(s.dev, dst, bytes, stream);
+    if (e != hipSuccess) return hip_fail(e, "stage_copy_kernel");
+  } else {
+    e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(plan)");
+  }
   e = hipEventRecord(s.done, stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
   s.pending = true;
@@ -665,6 +695,14 @@ struct TimingTotal {
   int64_t launches;
 };
 std::vector<TimingTotal> g_time_totals;
+std::vector<std::string> g_time_select;  // launch names to time; empty = every launch
+
+bool timing_selected_locked(const char* name) {
+  if (g_time_select.empty()) return true;
+  for (const auto& n : g_time_select)
+    if (n == name) return true;
+  return false;
+}
 
 hipEvent_t pool_get() {
   if (!g_event_pool.empty()) {
@@ -701,6 +739,7 @@ void drain_timing_locked() {
 TimingScope::TimingScope(const char* name, hipStream_t stream) : slot_(-1), stream_(stream) {
   if (!g_time_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lk(g_time_mu);
+  if (!timing_selected_locked(name)) return;
   hipEvent_t a = pool_get(), b = pool_get();
   if (!a || !b) return;
   if (hipEventRecord(a, stream) != hipSuccess) return;
@@ -1543,6 +1582,23 @@ pp_status pp_pack_export(const pp_pack_desc* desc, int block_q, int block_k, int
 
 pp_status pp_timing_enable(int on) {
   g_time_on.store(on != 0);
+  return PP_OK;
+}
+
+pp_status pp_timing_select(const char* names) {
+  std::vector<std::string> sel;
+  if (names) {
+    const char* c = names;
+    while (*c) {
+      const char* e = strchr(c, ',');
+      const size_t n = e ? (size_t)(e - c) : strlen(c);
+      if (n > 0) sel.emplace_back(c, n);
+      if (!e) break;
+      c = e + 1;
+    }
+  }
+  std::lock_guard<std::mutex> lk(g_time_mu);
+  g_time_select.swap(sel);
   return PP_OK;
 }
 

@@ -23,6 +23,10 @@ struct TimingScope {
   hipStream_t stream_;
 };
 
+// Copies `bytes` from src (the device address of mapped pinned host memory) to
+// device memory dst on stream s; both 16-byte aligned.
+hipError_t launch_stage_copy(const void* src, void* dst, size_t bytes, hipStream_t s);
+
 // fp32 -> bf16 (round to nearest even) copy, for fp32 callers of attention.
 hipError_t launch_to_bf16(const float* src, void* dst, int64_t n, hipStream_t s);
 

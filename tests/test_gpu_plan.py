@@ -99,3 +99,34 @@ def test_planned_full_size_workload_matches_self_contained():
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
     for a, b in zip(g1, g2):
         assert torch.equal(a, b)
+
+
+def test_timing_select_times_only_the_named_launches():
+    pack = _ragged()
+    q, k, v, do = wl.qkv(pack, 8, 2, 128, 501, torch.bfloat16, device=DEV)
+    print(f"case timing-select T={pack.total_tokens}", flush=True)
+    try:
+        pp.pp_timing_select(["pp_attn_fwd", "pp_attn_bwd_dq"])
+        pp.pp_timing_reset()
+        pp.pp_timing_enable(True)
+        for _ in range(3):
+            o, lse = pp.pp_attn_fwd(pack, q, k, v)
+            pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+        torch.cuda.synchronize()
+        pp.pp_timing_enable(False)
+        got = pp.pp_timing_get()
+        assert set(got) == {"pp_attn_fwd", "pp_attn_bwd_dq"}
+        assert all(n == 3 and ms > 0 for ms, n in got.values())
+        # back to every launch
+        pp.pp_timing_select(None)
+        pp.pp_timing_reset()
+        pp.pp_timing_enable(True)
+        o, lse = pp.pp_attn_fwd(pack, q, k, v)
+        pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+        torch.cuda.synchronize()
+        pp.pp_timing_enable(False)
+        assert {"pp_attn_fwd", "pp_attn_bwd_prep", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq"} <= set(pp.pp_timing_get())
+    finally:
+        pp.pp_timing_enable(False)
+        pp.pp_timing_select(None)
+        pp.pp_timing_reset()
