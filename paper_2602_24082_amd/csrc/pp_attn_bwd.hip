@@ -107,8 +107,10 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t 
     if (row < n_rows) {
       const int64_t h = row / p.sumT, t = row - h * p.sumT;
       const int64_t src = (t * p.hq + h) * D + part * 8;
-      a[k] = *reinterpret_cast<const vec8*>(p.dout_o + src);
-      b[k] = *reinterpret_cast<const vec8*>(p.o + src);
+      // each O and dO element is read once here: nontemporal loads (the dK/dV
+      // and dQ passes read dO as fast afterwards)
+      a[k] = __builtin_nontemporal_load(reinterpret_cast<const vec8*>(p.dout_o + src));
+      b[k] = __builtin_nontemporal_load(reinterpret_cast<const vec8*>(p.o + src));
     }
   }
 #pragma unroll

@@ -1308,6 +1308,7 @@ pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vo
   a.logits = logits;
   a.tokens = tokens;
   a.tok = tok_logp ? tok_logp : (float*)at(ws, p.lay, p.r_tok);
+  a.zero_tok = tok_logp != nullptr;
   a.seq = seq_logp;
   a.rows = (const LogitRowItem*)at(ws, p.lay, p.r_rows);
   a.labels = (const int32_t*)at(ws, p.lay, p.r_labels);
@@ -1474,10 +1475,16 @@ pp_status pp_dpo_loss(int32_t num_rows, int32_t max_resp, const int32_t* num_res
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "loss needs %zu workspace bytes, got %zu", need, ws_bytes);
   if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
   hipStream_t s = (hipStream_t)hip_stream;
-  pp_status st = stage_copy(ws, num_resp, (size_t)num_rows * 4, s);
-  if (st != PP_OK) return st;
   LossLaunch a{};
-  a.num_resp = (const int32_t*)ws;
+  if (num_rows <= kLossInlineRows) {
+    // few rows: the counts ride in the launch arguments, no copy
+    memcpy(a.nr_inline, num_resp, (size_t)num_rows * 4);
+    a.num_resp = nullptr;
+  } else {
+    pp_status st = stage_copy(ws, num_resp, (size_t)num_rows * 4, s);
+    if (st != PP_OK) return st;
+    a.num_resp = (const int32_t*)ws;
+  }
   a.pol = logp_pol;
   a.ref = logp_ref;
   a.beta = beta;

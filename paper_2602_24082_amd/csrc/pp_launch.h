@@ -103,7 +103,7 @@ hipError_t launch_rope(const RopeLaunch& a, hipStream_t s);
 struct LogprobLaunch {
   const void* logits;
   const int32_t* tokens;
-  float* tok;                // [sumT]; zero-filled, then response positions written
+  float* tok;                // [sumT]; response positions written (zero-filled first if zero_tok)
   float* seq;                // [B * K_max]
   const LogitRowItem* rows;
   const int32_t* labels;     // flat token positions
@@ -113,6 +113,9 @@ struct LogprobLaunch {
   int vocab;
   int sumT;
   int dtype;
+  // the caller's per-token output, whose other positions must read 0; workspace
+  // scratch is only read back at response positions, so it is not cleared
+  bool zero_tok;
 };
 hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s);
 
@@ -161,8 +164,11 @@ struct RmBwdLaunch {
 };
 hipError_t launch_rm_bwd(const RmBwdLaunch& a, hipStream_t s);
 
+// rows whose response counts travel inside the loss launch's arguments
+constexpr int kLossInlineRows = 256;
+
 struct LossLaunch {
-  const int32_t* num_resp;   // device copy [B]
+  const int32_t* num_resp;   // device copy [B], or null: counts in nr_inline
   const float* pol;
   const float* ref;          // may be null
   float beta;
@@ -171,6 +177,7 @@ struct LossLaunch {
   float* dlogp;              // may be null
   int B, K_max;
   int n_qualified;           // rows with K_b >= 2
+  int32_t nr_inline[kLossInlineRows];  // K_b when B <= kLossInlineRows
 };
 hipError_t launch_loss(const LossLaunch& a, hipStream_t s);
 

@@ -478,7 +478,7 @@ __global__ __launch_bounds__(256) void pair_loss_kernel(LossLaunch a) {
   const float inv_rows = 1.f / (float)a.n_qualified;
   float part = 0.f;
   for (int b = tid; b < a.B; b += blockDim.x) {
-    const int K = a.num_resp[b];
+    const int K = a.num_resp ? a.num_resp[b] : a.nr_inline[b];
     const float* pol = a.pol + (int64_t)b * a.K_max;
     const float* ref = a.ref ? a.ref + (int64_t)b * a.K_max : nullptr;
     float* g = a.dlogp ? a.dlogp + (int64_t)b * a.K_max : nullptr;
@@ -520,7 +520,7 @@ __global__ __launch_bounds__(256) void pair_loss_kernel(LossLaunch a) {
 }  // namespace
 
 hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s) {
-  if (a.sumT > 0) {
+  if (a.sumT > 0 && a.zero_tok) {
     TimingScope t("pp_fill_zero", s);
     hipLaunchKernelGGL(fill_zero_kernel, dim3((a.sumT + 255) / 256), dim3(256), 0, s, a.tok, a.sumT);
   }

@@ -241,6 +241,9 @@ def test_dpo_loss_and_bt_loss():
     _check_loss([4, 3, 1, 4, 0, 2], rng.standard_normal((6, 4)) * 10, None, 1.0)
     B = 700  # more rows than threads
     _check_loss(list(rng.integers(0, 5, B)), rng.standard_normal((B, 4)) * 5, rng.standard_normal((B, 4)) * 5, 0.5)
+    for B in (256, 257):  # the last row count passed in the launch arguments, the first one staged
+        _check_loss(list(rng.integers(0, 5, B)), rng.standard_normal((B, 4)) * 5, rng.standard_normal((B, 4)) * 5,
+                    0.3)
 
 
 def test_full_chain_tiny_config():
