@@ -38,6 +38,8 @@
 namespace pp {
 namespace {
 
+typedef uint32_t Chunk16 __attribute__((ext_vector_type(4)));
+
 template <typename TO>
 struct BwdParams {
   const __bf16* q;
@@ -62,6 +64,13 @@ struct BwdParams {
   float scale_log2;
   const int32_t* pos;      // ROPE: position of every flat token
   const double* inv_freq;  // ROPE: [D/2]
+  // plan metadata copied by the pre-pass's workgroups from prep_blocks on:
+  // 16-byte vectors [0, stage_n16), then stage_tail (< 16) single bytes
+  const Chunk16* stage_src;
+  Chunk16* stage_dst;
+  int64_t stage_n16;
+  int stage_tail;
+  int64_t prep_blocks;
 };
 
 // Inverse rotary rotation of one lane's gradient row held in 32x32 accumulator
@@ -90,6 +99,16 @@ constexpr int kPrepRowsPerThread = 4;
 
 template <int D, typename TO>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t n_rows) {
+  if (blockIdx.x >= p.prep_blocks) {
+    // the plan metadata copy (the dK/dV and dQ passes, launched after this
+    // kernel, read it; this pass does not)
+    const int64_t i = (blockIdx.x - p.prep_blocks) * 256 + threadIdx.x;
+    if (i < p.stage_n16) p.stage_dst[i] = p.stage_src[i];
+    if (i < p.stage_tail)
+      reinterpret_cast<uint8_t*>(p.stage_dst + p.stage_n16)[i] =
+          reinterpret_cast<const uint8_t*>(p.stage_src + p.stage_n16)[i];
+    return;
+  }
   constexpr int LPR = D / 8;      // lanes per (token, head) row
   constexpr int RPB = 256 / LPR;  // rows per block and pass
   constexpr int RPT = kPrepRowsPerThread;
@@ -543,8 +562,15 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   if (n_rows == 0) return hipSuccess;
   {
     constexpr int RPB = 256 / (D / 8) * kPrepRowsPerThread;
+    p.prep_blocks = (n_rows + RPB - 1) / RPB;
+    p.stage_src = static_cast<const Chunk16*>(a.stage_src);
+    p.stage_dst = static_cast<Chunk16*>(a.stage_dst);
+    p.stage_n16 = (int64_t)(a.stage_bytes / 16);
+    p.stage_tail = (int)(a.stage_bytes % 16);
+    const int64_t copy_threads = p.stage_n16 > p.stage_tail ? p.stage_n16 : p.stage_tail;
+    const int64_t copy_blocks = a.stage_bytes ? (copy_threads + 255) / 256 : 0;
     TimingScope t("pp_attn_bwd_prep", s);
-    hipLaunchKernelGGL((bwd_prep_kernel<D, TO>), dim3((unsigned)((n_rows + RPB - 1) / RPB)), dim3(256), 0, s,
+    hipLaunchKernelGGL((bwd_prep_kernel<D, TO>), dim3((unsigned)(p.prep_blocks + copy_blocks)), dim3(256), 0, s,
                        p, n_rows);
   }
   hipError_t e = hipGetLastError();

@@ -457,11 +457,18 @@ struct StagingRelease {
   }
 } g_stage_release;
 
-// Copies `bytes` from `src` into device memory `dst` (on the current device,
-// whose stream `stream` is) through a pinned slot of that device's ring: the
-// host fills the slot and a kernel on `stream` copies it into `dst`.
-pp_status stage_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
-  if (bytes == 0) return PP_OK;
+// Stages `bytes` from `src` for device memory `dst` (on the current device,
+// whose stream `stream` is) through a pinned slot of that device's ring, then
+// calls `launch(dev_src)`, which enqueues the work that needs the data: with a
+// mapped slot and a 16-byte aligned `dst`, dev_src is the slot's device address
+// and a kernel that `launch` enqueues must copy it into `dst` before any kernel
+// reads `dst`; otherwise the data is already on its way by hipMemcpyAsync and
+// dev_src is null.  The slot's
+// event is recorded after `launch` in every case, so the slot is not reused
+// while a kernel may still read it.
+template <typename Launch>
+pp_status stage_with(void* dst, const void* src, size_t bytes, hipStream_t stream, Launch&& launch) {
+  if (bytes == 0) return launch(nullptr);
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice(staging)");
@@ -492,17 +499,28 @@ pp_status stage_copy(void* dst, const void* src, size_t bytes, hipStream_t strea
     else (void)hipGetLastError();  // no mapped address: this slot copies with hipMemcpyAsync
   }
   memcpy(s.host, src, bytes);
+  const void* dev_src = nullptr;
   if (s.dev && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
-    e = launch_stage_copy(s.dev, dst, bytes, stream);
-    if (e != hipSuccess) return hip_fail(e, "stage_copy_kernel");
+    dev_src = s.dev;
   } else {
     e = hipMemcpyAsync(dst, s.host, bytes, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(plan)");
   }
+  const pp_status st = launch(dev_src);
   e = hipEventRecord(s.done, stream);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
   s.pending = true;
-  return PP_OK;
+  return st;
+}
+
+// Copies `bytes` from `src` into device memory `dst` on `stream` (a copy kernel
+// from the mapped slot, or hipMemcpyAsync).
+pp_status stage_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+  return stage_with(dst, src, bytes, stream, [&](const void* dev_src) -> pp_status {
+    if (!dev_src) return PP_OK;
+    hipError_t e = launch_stage_copy(dev_src, dst, bytes, stream);
+    return e == hipSuccess ? PP_OK : hip_fail(e, "stage_copy_kernel");
+  });
 }
 
 // Serialises regions into one host image of the metadata prefix.
@@ -974,10 +992,12 @@ void bwd_image(const Batch& bt, const BwdPlan& p, int head_dim, const double* ro
 }
 
 // Enqueues the backward on metadata already staged in ws.
+// stage_src / stage_bytes: metadata still to be copied into ws (by the delta
+// pre-pass, which reads none of it), or null.
 pp_status bwd_launch(const BwdPlan& p, void* ws, int sumT, pp_dtype dtype, int hq, int hkv, int head_dim,
                      float scale, const void* q, const void* k, const void* v, const void* o,
                      const float* lse, const void* dout, void* dq, void* dk, void* dv, bool rope,
-                     hipStream_t s) {
+                     hipStream_t s, const void* stage_src = nullptr, size_t stage_bytes = 0) {
   hipError_t e;
   const void* dout_bf = dout;
   if (p.cast.on) {
@@ -1026,6 +1046,9 @@ pp_status bwd_launch(const BwdPlan& p, void* ws, int sumT, pp_dtype dtype, int h
     a.pos = (const int32_t*)at(ws, p.lay, p.r_pos);
     a.inv_freq = (const double*)at(ws, p.lay, p.r_freq);
   }
+  a.stage_src = stage_src;
+  a.stage_dst = ws;
+  a.stage_bytes = stage_src ? stage_bytes : 0;
   e = launch_attn_bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "attention backward launch");
   return PP_OK;
@@ -1054,9 +1077,11 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   const double base = rope_base ? *rope_base : 0.0;
   bwd_image(bt, p, head_dim, rope_base ? &base : nullptr, &img);
   hipStream_t s = (hipStream_t)hip_stream;
-  if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
-  return bwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, dout, dq, dk, dv,
-                    rope_base != nullptr, s);
+  // the metadata copy rides in the delta pre-pass's launch
+  return stage_with(ws, img.buf.data(), img.buf.size(), s, [&](const void* dev_src) {
+    return bwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, dout, dq, dk, dv,
+                      rope_base != nullptr, s, dev_src, img.buf.size());
+  });
 }
 
 // Workspace of pp_rope: positions then frequencies.

@@ -84,6 +84,11 @@ struct AttnBwdLaunch {
   bool rope = false;
   const int32_t* pos = nullptr;
   const double* inv_freq = nullptr;
+  // plan metadata to copy into stage_dst (16-byte aligned) from mapped pinned
+  // host memory, done by extra workgroups of the delta pre-pass; none if 0 bytes
+  const void* stage_src = nullptr;
+  void* stage_dst = nullptr;
+  size_t stage_bytes = 0;
 };
 hipError_t launch_attn_bwd(const AttnBwdLaunch& a, hipStream_t s);
 
