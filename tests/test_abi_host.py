@@ -330,3 +330,12 @@ def test_plan_argument_checks():
     assert L.pp_attn_fwd_planned(h, 0.0, ok, ok, ctypes.c_void_p(4096 + 8), ok, ok, None, None, None) == 1
     assert L.pp_attn_bwd_planned(h, 0.0, ok, ok, ok, ok, ok, ok, ok, ok, ok, None) == 0
     assert L.pp_plan_destroy(h) == 0
+
+
+def test_timing_select_accepts_lists():
+    L = binding.lib()
+    for arg in (None, b"", b"pp_attn_fwd", b"pp_attn_fwd,pp_logprob_rows", b",pp_attn_bwd_dq,,", b","):
+        assert L.pp_timing_select(arg) == 0, arg
+    assert L.pp_timing_select(None) == 0
+    # nothing was launched, so nothing was timed
+    assert L.pp_timing_reset() == 0 and L.pp_timing_count() == 0
