@@ -14,6 +14,7 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
+from tolerances import o_excess
 
 pytestmark = pytest.mark.gpu
 
@@ -47,7 +48,7 @@ def _attention_sample(cfg_index, group):
     dq_r, dk_r, dv_r = orc.attn_bwd(*args, sub(q, hs), sub(k, gs), sub(v, gs), sub(do, hs))
     o_c = sub(o, hs)
     l_c = lse[hs, r0:r1].double().cpu().numpy()
-    assert np.abs(o_c - O_ref).max() <= 1e-2
+    assert o_excess(o_c, O_ref, True) <= 0, np.abs(o_c - O_ref).max()
     assert np.abs(l_c - L_ref).max() <= 1e-2
     for name, got, ref in (("dq", sub(dq, hs), dq_r), ("dk", sub(dk, gs), dk_r), ("dv", sub(dv, gs), dv_r)):
         err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
@@ -100,7 +101,7 @@ def _attention_rope_sample(cfg_index, group, base):
     qb, kb = to_bf(qr), to_bf(kr)
     O_ref, L_ref = orc.attn_fwd(*args, qb, kb, sub(v, gs))
     dqr, dkr, dv_r = orc.attn_bwd(*args, qb, kb, sub(v, gs), sub(do, hs))
-    assert np.abs(sub(o, hs) - O_ref).max() <= 1e-2
+    assert o_excess(sub(o, hs), O_ref, True) <= 0, np.abs(sub(o, hs) - O_ref).max()
     assert np.abs(lse[hs, r0:r1].double().cpu().numpy() - L_ref).max() <= 1e-2
     for name, got, ref in (("dq", sub(dq, hs), orc.pack_rope(*args, dqr, base, inverse=True)),
                            ("dk", sub(dk, gs), orc.pack_rope(*args, dkr, base, inverse=True)),

@@ -84,6 +84,27 @@ def test_logprob_bwd_register_row_limit():
     _check_bwd(pack, 65540, torch.float32, 3.0, 186)
 
 
+def _random_logprob_pack(rng):
+    B = int(rng.integers(1, 5))
+    P, L, pad = [], [], []
+    for _ in range(B):
+        P.append(int(rng.integers(1, 200)))
+        L.append([int(x) for x in rng.integers(0, 120, size=int(rng.integers(0, 5)))])
+        pad.append(int(rng.integers(0, 9)))
+    return wl.make_pack(P, L, pad=pad)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_logprob_bwd_random_sweep(seed):
+    """Seeded random packs and vocabularies (the register-row and the two-read
+    kernel, aligned and unaligned rows), bf16 and fp32."""
+    rng = np.random.default_rng(4000 + seed)
+    pack = _random_logprob_pack(rng)
+    V = int(rng.choice([1000, 4099, 32000, 50257, 70000]))
+    dtype = torch.bfloat16 if seed % 2 == 0 else torch.float32
+    _check_bwd(pack, V, dtype, 3.0, 4100 + seed)
+
+
 def test_logprob_bwd_takes_the_loss_gradient():
     # the DPO chain: forward scores, loss gradient, then logits gradient
     pack = wl.make_pack([30, 12, 20], [[10, 14], [7, 9], [5, 6]])

@@ -1,7 +1,7 @@
 """GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
 
 Tolerances (attention in bf16 MFMA with fp32 accumulation):
-  O            max |O - O_ref|                          <= 1e-2
+  O            max |O - O_ref| <= 1e-2 (+ half a bf16 ulp of O_ref for bf16 O; tolerances.py)
   LSE          max |lse - lse_ref|                      <= 1e-2
   dQ, dK, dV   ||g - g_ref||_F / ||g_ref||_F            <= 2e-2 (each)
   seq log-prob |s - s_ref| / |s_ref|                    <= 1e-4
@@ -19,11 +19,11 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
+from tolerances import o_excess
 
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-O_TOL = 1e-2
 LSE_TOL = 1e-2
 G_TOL = 2e-2
 LP_TOL = 1e-4
@@ -58,7 +58,7 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
     o_c = o.double().cpu().numpy()
     l_c = lse.double().cpu().numpy()
     assert np.isfinite(o_c).all() and np.isfinite(l_c).all(), "unwritten output"
-    assert np.abs(o_c - O_ref).max() <= O_TOL, np.abs(o_c - O_ref).max()
+    assert o_excess(o_c, O_ref, dtype == torch.bfloat16) <= 0, np.abs(o_c - O_ref).max()
     assert np.abs(l_c - L_ref).max() <= LSE_TOL, np.abs(l_c - L_ref).max()
     if not check_bwd:
         return
@@ -109,6 +109,31 @@ def test_edge_cases():
     _check_attention(pack, 4, 1, 64, torch.bfloat16, 41)
     pack = wl.make_pack([5, 0], [[], []], pad=[0, 9])  # all-padding second row
     _check_attention(pack, 2, 2, 128, torch.bfloat16, 42)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_pack_sweep(seed):
+    """Seeded random packs: prompt lengths 0-400 (the first row has none on two
+    seeds: its responses are then separate documents), 0-4 responses of 0-260
+    tokens, 0-20 padding tokens, GQA ratios 1, 2, 4 and 8, d 64 or 128; forward
+    and all three gradients against the oracle."""
+    rng = np.random.default_rng(1000 + seed)
+    B = int(rng.integers(1, 5))
+    P, L, pad = [], [], []
+    for _ in range(B):
+        k = int(rng.integers(0, 5))
+        lens = [int(x) for x in rng.integers(0, 261, size=k)]
+        p0 = int(rng.integers(0, 401))
+        P.append(p0)
+        L.append(lens)
+        pad.append(int(rng.integers(0, 21)))
+    if seed % 4 == 3:
+        P[0], L[0] = 0, [17, 40]
+    pack = wl.make_pack(P, L, pad=pad)
+    hkv = int(rng.choice([1, 2, 4]))
+    G = int(rng.choice([1, 2, 4, 8]))
+    d = int(rng.choice([64, 128]))
+    _check_attention(pack, hkv * G, hkv, d, torch.bfloat16, 2000 + seed)
 
 
 def test_large_scores():
@@ -194,6 +219,27 @@ def _check_logprob(pack, V, dtype, sigma, seed):
     assert rel.max() <= LP_TOL, rel.max()
     assert np.abs(t - ref_tok).max() <= 1e-4 * max(1.0, np.abs(ref_tok).max())
     return s
+
+
+def _random_logprob_pack(rng):
+    B = int(rng.integers(1, 5))
+    P, L, pad = [], [], []
+    for _ in range(B):
+        P.append(int(rng.integers(1, 200)))
+        L.append([int(x) for x in rng.integers(0, 120, size=int(rng.integers(0, 5)))])
+        pad.append(int(rng.integers(0, 9)))
+    return wl.make_pack(P, L, pad=pad)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_logprob_random_sweep(seed):
+    """Seeded random packs and vocabularies (rows 16-byte aligned or not), bf16
+    and fp32 logits, against the oracle's per-response log-probabilities."""
+    rng = np.random.default_rng(3000 + seed)
+    pack = _random_logprob_pack(rng)
+    V = int(rng.choice([1000, 4099, 32000, 50257]))
+    dtype = torch.bfloat16 if seed % 2 == 0 else torch.float32
+    _check_logprob(pack, V, dtype, 3.0, 3100 + seed)
 
 
 def test_logprob_tiny_fp32():

@@ -4,7 +4,8 @@ The planned calls run the same kernels on the same metadata as the
 self-contained entry points, so their outputs must be bit-identical to
 pp_attn_fwd / pp_attn_bwd (and the rotary variants) for the same inputs; one
 case is also checked against the oracle directly, at the attention tolerances
-(O, LSE max-abs <= 1e-2; dQ, dK, dV relative Frobenius <= 2e-2).  A plan is
+(O max-abs <= 1e-2 beyond its bf16 rounding, LSE max-abs <= 1e-2; dQ, dK, dV relative
+Frobenius <= 2e-2).  A plan is
 reused for several "layers" (different q, k, v) and does not depend on the
 caller's descriptor arrays after creation.
 """
@@ -15,6 +16,7 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
+from tolerances import o_excess
 
 pytestmark = pytest.mark.gpu
 
@@ -59,7 +61,7 @@ def test_planned_matches_oracle():
     args = pack.oracle_args()
     qn, kn, vn, don = (x.double().numpy() for x in (q, k, v, do))
     O, L = orc.attn_fwd(*args, qn, kn, vn)
-    assert np.abs(o.double().cpu().numpy() - O).max() <= 1e-2
+    assert o_excess(o.double().cpu().numpy(), O, True) <= 0
     assert np.abs(lse.double().cpu().numpy() - L).max() <= 1e-2
     for got, ref in zip((dq, dk, dv), orc.attn_bwd(*args, qn, kn, vn, don)):
         g = got.double().cpu().numpy()

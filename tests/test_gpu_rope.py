@@ -9,7 +9,7 @@ Tolerances:
                   of the fp32 result, 2^-9 relative, plus fp32 products and
                   sine/cosine good to ~1e-7)
                   |y - y_ref| <= 4e-6 max|x|                  (fp32 outputs)
-  O, LSE          max-abs <= 1e-2; dQ, dK, dV relative Frobenius <= 2e-2 (the
+  O, LSE          max-abs <= 1e-2 (O: beyond its bf16 rounding, tolerances.py); dQ, dK, dV relative Frobenius <= 2e-2 (the
                   attention tolerances; dq and dk are w.r.t. the un-rotated q, k)
 
 The rotated queries and keys are bf16 activations, as in a bf16 model: the
@@ -27,6 +27,7 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
+from tolerances import o_excess
 
 pytestmark = pytest.mark.gpu
 
@@ -90,7 +91,7 @@ def _check_fused(pack, hq, hkv, d, base, dtype, seed):
     O_ref, L_ref = orc.attn_fwd(*args, qr_b, kr_b, vn)
     o_c, l_c = o.double().cpu().numpy(), lse.double().cpu().numpy()
     assert np.isfinite(o_c).all() and np.isfinite(l_c).all()
-    assert np.abs(o_c - O_ref).max() <= O_TOL, np.abs(o_c - O_ref).max()
+    assert o_excess(o_c, O_ref, dtype == torch.bfloat16) <= 0, np.abs(o_c - O_ref).max()
     assert np.abs(l_c - L_ref).max() <= O_TOL, np.abs(l_c - L_ref).max()
     bf = dtype == torch.bfloat16
     _check_rot(q_rot, qr_ref, np.abs(qn).max(), bf)
