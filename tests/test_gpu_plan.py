@@ -132,3 +132,44 @@ def test_timing_select_times_only_the_named_launches():
         pp.pp_timing_enable(False)
         pp.pp_timing_select(None)
         pp.pp_timing_reset()
+
+
+def test_self_contained_calls_from_two_threads():
+    """Two host threads, each on its own stream, call the self-contained entry
+    points (which stage their metadata through the shared pinned ring) over and
+    over; every result equals the single-threaded one bit for bit."""
+    import threading
+    packs = [_ragged(), wl.make_pack([500, 77], [[100, 28, 300], [64, 64]], pad=[0, 5])]
+    hq, hkv, d = 8, 2, 128
+    inputs = [wl.qkv(pk, hq, hkv, d, 600 + i, torch.bfloat16, device=DEV) for i, pk in enumerate(packs)]
+    print(f"case two-threads T={[pk.total_tokens for pk in packs]}", flush=True)
+
+    def run(i):
+        q, k, v, do = inputs[i]
+        o, lse = pp.pp_attn_fwd(packs[i], q, k, v)
+        return (o, lse, *pp.pp_attn_bwd(packs[i], q, k, v, o, lse, do))
+
+    want = [run(i) for i in range(2)]
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream(device=DEV)
+            with torch.cuda.stream(s):
+                for _ in range(12):
+                    got = run(i)
+                    s.synchronize()
+                    if not all(torch.equal(a, b) for a, b in zip(got, want[i])):
+                        errors.append(f"thread {i}: result differs")
+                        return
+        except Exception as e:  # surfaced below
+            errors.append(f"thread {i}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a worker did not finish"
+    assert not errors, errors
