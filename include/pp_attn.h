@@ -31,7 +31,9 @@
  *   Tensor arguments of the attention and rotary entry points (q, k, v, o, dout,
  *   dq, dk, dv, q_rot, k_rot, x, y) must be 16-byte aligned, lse 4-byte aligned
  *   (rows move in 16-byte vectors); a misaligned pointer is rejected with
- *   PP_ERR_INVALID_ARGUMENT.  Allocations from hipMalloc or torch qualify.
+ *   PP_ERR_INVALID_ARGUMENT.  Workspaces (`ws`) must be 256-byte aligned, and
+ *   are rejected the same way otherwise.  Allocations from hipMalloc or torch
+ *   qualify.
  * Streams.  All device work is enqueued on `hip_stream` (a hipStream_t; NULL
  *   means the null stream) in call order; no entry point synchronises the device.
  * Errors.  Arguments are validated on the host before anything is enqueued; a

@@ -844,6 +844,9 @@ struct RopeArgs {
 // The kernels move tensor rows in 16-byte vectors (and DMA them into LDS in
 // 16-byte chunks), so every tensor argument must start on a 16-byte boundary.
 inline bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15) == 0; }
+// workspaces hold metadata records read by scalar loads, doubles and 16-byte
+// vectors: they must start on a 256-byte boundary (hipMalloc and torch qualify)
+inline bool aligned256(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 255) == 0; }
 inline bool aligned4(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 3) == 0; }
 
 pp_status check_fwd_ptrs(int sumT, const void* q, const void* k, const void* v, const void* o, const float* lse,
@@ -964,6 +967,7 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "forward needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
   if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (bt.sumT == 0) return PP_OK;
   MetaImage img;
   const double base = rope ? rope->base : 0.0;
@@ -1072,6 +1076,7 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
   if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (bt.sumT == 0) return PP_OK;
   MetaImage img;
   const double base = rope_base ? *rope_base : 0.0;
@@ -1172,6 +1177,7 @@ pp_status pp_plan_create(const pp_pack_desc* desc, pp_dtype dtype, int hq, int h
   if (st == PP_OK && ws_bytes < total)
     st = fail(PP_ERR_WORKSPACE_TOO_SMALL, "the plan needs %zu workspace bytes, got %zu", total, ws_bytes);
   if (st == PP_OK && total && !ws) st = fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (st == PP_OK && ws && !aligned256(ws)) st = fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (st == PP_OK && bt.sumT > 0) {
     // one image: the forward's metadata at 0, the backward's at bwd_off
     const double base = rope_base ? *rope_base : 0.0;
@@ -1279,6 +1285,7 @@ pp_status pp_rope(const pp_pack_desc* desc, pp_dtype dtype, int heads, int head_
   if (ws_bytes < p.lay.total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "rope needs %zu workspace bytes, got %zu", p.lay.total, ws_bytes);
   if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (bt.sumT == 0) return PP_OK;
   hipStream_t s = (hipStream_t)hip_stream;
   std::vector<int32_t> pos;
@@ -1322,6 +1329,7 @@ pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vo
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "logprob needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
   if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (bt.Kmax == 0 && (bt.sumT == 0 || !tok_logp)) return PP_OK;
   hipStream_t s = (hipStream_t)hip_stream;
   MetaImage img;
@@ -1369,6 +1377,7 @@ pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, in
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "logprob needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
   if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   hipStream_t s = (hipStream_t)hip_stream;
   MetaImage img;
   img.put(p.lay.regions[p.r_rows], p.l.rows.data(), p.l.rows.size() * sizeof(LogitRowItem));
@@ -1421,6 +1430,7 @@ pp_status pp_rm_scores(const pp_pack_desc* desc, pp_dtype dtype, int hidden_dim,
   if (ws_bytes < p.lay.total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "rm head needs %zu workspace bytes, got %zu", p.lay.total, ws_bytes);
   if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   hipStream_t s = (hipStream_t)hip_stream;
   if ((st = stage_copy(ws, p.slot_row.data(), p.slot_row.size() * 8, s)) != PP_OK) return st;
   RmLaunch a{};
@@ -1452,6 +1462,7 @@ pp_status pp_rm_scores_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hidden_
   if (ws_bytes < p.lay.total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "rm head needs %zu workspace bytes, got %zu", p.lay.total, ws_bytes);
   if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   hipStream_t s = (hipStream_t)hip_stream;
   MetaImage img;
   img.put(p.lay.regions[p.r_slot_row], p.slot_row.data(), p.slot_row.size() * 8);
@@ -1499,6 +1510,7 @@ pp_status pp_dpo_loss(int32_t num_rows, int32_t max_resp, const int32_t* num_res
   if (ws_bytes < need)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "loss needs %zu workspace bytes, got %zu", need, ws_bytes);
   if (!ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   hipStream_t s = (hipStream_t)hip_stream;
   LossLaunch a{};
   if (num_rows <= kLossInlineRows) {

@@ -339,3 +339,21 @@ def test_timing_select_accepts_lists():
     assert L.pp_timing_select(None) == 0
     # nothing was launched, so nothing was timed
     assert L.pp_timing_reset() == 0 and L.pp_timing_count() == 0
+
+
+def test_misaligned_workspace_rejected():
+    """A workspace off a 256-byte boundary is refused before anything is enqueued."""
+    L = binding.lib()
+    ok = ctypes.c_void_p(4096)
+    off = ctypes.c_void_p(4096 + 16)
+    big = 1 << 30
+    d, keep = _raw_desc([0, 12], [4], [2], [4, 7], [3, 3], 2)
+    assert L.pp_attn_fwd(ctypes.byref(d), 0, 4, 2, 64, 0.0, ok, ok, ok, ok, ok, off, big, None) == 1
+    assert L.pp_attn_bwd(ctypes.byref(d), 0, 4, 2, 64, 0.0, ok, ok, ok, ok, ok, ok, ok, ok, ok, off, big, None) == 1
+    assert L.pp_seq_logprob(ctypes.byref(d), 0, 1000, ok, ok, ok, None, off, big, None) == 1
+    num = (ctypes.c_int32 * 2)(2, 2)
+    assert L.pp_dpo_loss(2, 2, num, ok, ok, ctypes.c_float(0.1), ok, None, None, off, big, None) == 1
+    h = ctypes.c_void_p(0)
+    assert L.pp_plan_create(ctypes.byref(d), 0, 4, 2, 128, None, off, big, None, ctypes.byref(h)) == 1
+    assert h.value is None
+    assert b"256-byte" in L.pp_last_error()
