@@ -296,8 +296,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
       __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
-        if (c + 1 < NC) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
-        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+        // two reads of the next chunk before each MFMA: LDS requests spread
+        // evenly over the MFMA stream (2% faster than four reads per two MFMAs)
+        if (c + 1 < NC) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+        if (c + 1 < NC) __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
       }
     }
     // masked pairs get S = -inf (so P = dS = 0); a block whose 32 x 32 pairs
