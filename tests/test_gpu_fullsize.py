@@ -5,7 +5,13 @@ configuration the benchmark times; the fp64 oracle then recomputes a sample
 it can afford -- one row (rows are independent) and one kv-head group (heads
 are independent), or single responses for the log-probabilities -- and the
 two are compared element by element with the same tolerances as the small
-parity tests.
+parity tests, gradients also per prompt and per response (gradcheck.py).
+
+Attention is sampled on the longest row of the 8B-shaped, reward-model and
+DPO-chain batches (the longest prompt key ranges: their key tiles walk the most
+query steps and gather the most responses) and on the shortest; on the
+long-prefix batch, whose longest row (6348 tokens) would hold the oracle for
+minutes, on the row of median length and the shortest.
 """
 import numpy as np
 import pytest
@@ -14,7 +20,8 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
-from tolerances import o_excess
+from gradcheck import check_grad
+from tolerances import lse_excess, o_excess, rope_lse_slack
 
 pytestmark = pytest.mark.gpu
 
@@ -27,7 +34,16 @@ def _row_pack(pack, b):
                         pad=[int(pack.row_lengths()[b]) - int(pack.prompt_len[b]) - int(pack.resp_len[b, :K].sum())])
 
 
-def _attention_sample(cfg_index, group):
+def _pick_row(pack, which):
+    n = pack.row_lengths()
+    if which == "shortest":
+        return int(np.argmin(n))
+    if which == "longest":
+        return int(np.argmax(n))
+    return int(np.argsort(n, kind="stable")[len(n) // 2])  # median length
+
+
+def _attention_sample(cfg_index, group, which):
     cfg = wl.CONFIGS[cfg_index]
     pack = wl.config_pack(cfg)
     seed = wl.tensor_seed(cfg.index, 0)
@@ -35,12 +51,13 @@ def _attention_sample(cfg_index, group):
     o, lse = pp.pp_attn_fwd(pack, q, k, v)
     dq, dk, dv = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
     torch.cuda.synchronize()
-    b = int(np.argmin(pack.row_lengths()))        # the shortest row keeps the oracle cheap
+    b = _pick_row(pack, which)
     r0, r1 = int(pack.row_start[b]), int(pack.row_start[b + 1])
     G = cfg.hq // cfg.hkv
     hs = slice(group * G, (group + 1) * G)
     gs = slice(group, group + 1)
-    print(f"{cfg.name}: row {b} T={r1 - r0}, q-heads {hs.start}..{hs.stop - 1}, kv-head {group}", flush=True)
+    print(f"{cfg.name}: {which} row {b} T={r1 - r0}, q-heads {hs.start}..{hs.stop - 1}, kv-head {group}",
+          flush=True)
     sub = lambda x, s: x[r0:r1, s].double().cpu().numpy()
     row = _row_pack(pack, b)
     args = row.oracle_args()
@@ -49,29 +66,34 @@ def _attention_sample(cfg_index, group):
     o_c = sub(o, hs)
     l_c = lse[hs, r0:r1].double().cpu().numpy()
     assert o_excess(o_c, O_ref, True) <= 0, np.abs(o_c - O_ref).max()
-    assert np.abs(l_c - L_ref).max() <= 1e-2
+    assert lse_excess(l_c, L_ref) <= 0, np.abs(l_c - L_ref).max()
+    print(f"  max|dO| {np.abs(o_c - O_ref).max():.3e}  max|dLSE| {np.abs(l_c - L_ref).max():.3e}", flush=True)
     for name, got, ref in (("dq", sub(dq, hs), dq_r), ("dk", sub(dk, gs), dk_r), ("dv", sub(dv, gs), dv_r)):
-        err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
-        assert err <= 2e-2, (name, err)
+        worst = check_grad(row, name, got, ref)
+        print(f"  {name}: worst whole/segment rel. Frobenius {worst:.3e}", flush=True)
     # nothing left unwritten anywhere in the batch
     for t in (o, lse, dq, dk, dv):
         assert torch.isfinite(t).all()
 
 
-def test_fullsize_llama3_8b_attention():
-    _attention_sample(1, group=3)
+@pytest.mark.parametrize("which", ["longest", "shortest"])
+def test_fullsize_llama3_8b_attention(which):
+    _attention_sample(1, group=3, which=which)
 
 
-def test_fullsize_rm_k4_attention():
-    _attention_sample(2, group=5)
+@pytest.mark.parametrize("which", ["longest", "shortest"])
+def test_fullsize_rm_k4_attention(which):
+    _attention_sample(2, group=5, which=which)
 
 
-def test_fullsize_long_prefix_attention():
-    _attention_sample(3, group=7)
+@pytest.mark.parametrize("which", ["median", "shortest"])
+def test_fullsize_long_prefix_attention(which):
+    _attention_sample(3, group=7, which=which)
 
 
-def test_fullsize_dpo_chain_attention():
-    _attention_sample(4, group=0)
+@pytest.mark.parametrize("which", ["longest", "shortest"])
+def test_fullsize_dpo_chain_attention(which):
+    _attention_sample(4, group=0, which=which)
 
 
 def _attention_rope_sample(cfg_index, group, base):
@@ -85,14 +107,15 @@ def _attention_rope_sample(cfg_index, group, base):
     o, lse, q_rot, k_rot = pp.pp_attn_fwd_rope(pack, q, k, v, base)
     dq, dk, dv = pp.pp_attn_bwd_rope(pack, q_rot, k_rot, v, o, lse, do, base)
     torch.cuda.synchronize()
-    b = int(np.argmin(pack.row_lengths()))
+    b = _pick_row(pack, "shortest")
     r0, r1 = int(pack.row_start[b]), int(pack.row_start[b + 1])
     G = cfg.hq // cfg.hkv
     hs = slice(group * G, (group + 1) * G)
     gs = slice(group, group + 1)
     print(f"{cfg.name} rope base {base}: row {b} T={r1 - r0}, kv-head {group}", flush=True)
     sub = lambda x, s: x[r0:r1, s].double().cpu().numpy()
-    args = _row_pack(pack, b).oracle_args()
+    row = _row_pack(pack, b)
+    args = row.oracle_args()
     qr = orc.pack_rope(*args, sub(q, hs), base)
     kr = orc.pack_rope(*args, sub(k, gs), base)
     for got, ref in ((sub(q_rot, hs), qr), (sub(k_rot, gs), kr)):
@@ -102,12 +125,12 @@ def _attention_rope_sample(cfg_index, group, base):
     O_ref, L_ref = orc.attn_fwd(*args, qb, kb, sub(v, gs))
     dqr, dkr, dv_r = orc.attn_bwd(*args, qb, kb, sub(v, gs), sub(do, hs))
     assert o_excess(sub(o, hs), O_ref, True) <= 0, np.abs(sub(o, hs) - O_ref).max()
-    assert np.abs(lse[hs, r0:r1].double().cpu().numpy() - L_ref).max() <= 1e-2
+    slack = rope_lse_slack(row, qr, kr, 4e-6 * np.abs(sub(q, hs)).max(), 4e-6 * np.abs(sub(k, gs)).max())
+    assert lse_excess(lse[hs, r0:r1].double().cpu().numpy(), L_ref, slack) <= 0
     for name, got, ref in (("dq", sub(dq, hs), orc.pack_rope(*args, dqr, base, inverse=True)),
                            ("dk", sub(dk, gs), orc.pack_rope(*args, dkr, base, inverse=True)),
                            ("dv", sub(dv, gs), dv_r)):
-        err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
-        assert err <= 2e-2, (name, err)
+        check_grad(row, name, got, ref)
     for t in (o, lse, dq, dk, dv, q_rot, k_rot):
         assert torch.isfinite(t).all()
 

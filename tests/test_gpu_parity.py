@@ -2,8 +2,9 @@
 
 Tolerances (attention in bf16 MFMA with fp32 accumulation):
   O            max |O - O_ref| <= 1e-2 (+ half a bf16 ulp of O_ref for bf16 O; tolerances.py)
-  LSE          max |lse - lse_ref|                      <= 1e-2
-  dQ, dK, dV   ||g - g_ref||_F / ||g_ref||_F            <= 2e-2 (each)
+  LSE          max |lse - lse_ref| <= 2e-4 + 2^-16 |lse_ref|  (fp32 arithmetic; tolerances.py)
+  dQ, dK, dV   ||g - g_ref||_F / ||g_ref||_F <= 2e-2, each, over the whole tensor AND
+               over every prompt's and every response's rows (gradcheck.py)
   seq log-prob |s - s_ref| / |s_ref|                    <= 1e-4
   loss, dlogp  relative                                 <= 1e-4
 The oracle runs on the inputs the kernels see: bf16 inputs as rounded, fp32
@@ -19,24 +20,18 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
-from tolerances import o_excess
+from gradcheck import check_grad
+from tolerances import fp32_lse_slack, lse_excess, o_excess
 
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-LSE_TOL = 1e-2
-G_TOL = 2e-2
 LP_TOL = 1e-4
 
 
 def _inputs(pack, hq, hkv, d, dtype, seed):
     q, k, v, do = wl.qkv(pack, hq, hkv, d, seed, dtype, device="cpu")
     return q, k, v, do
-
-
-def _rel_fro(a, b):
-    n = np.linalg.norm(b)
-    return np.linalg.norm(a - b) / max(n, 1e-30)
 
 
 def _poisoned_like(t):
@@ -59,18 +54,23 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
     l_c = lse.double().cpu().numpy()
     assert np.isfinite(o_c).all() and np.isfinite(l_c).all(), "unwritten output"
     assert o_excess(o_c, O_ref, dtype == torch.bfloat16) <= 0, np.abs(o_c - O_ref).max()
-    assert np.abs(l_c - L_ref).max() <= LSE_TOL, np.abs(l_c - L_ref).max()
+    # fp32 callers: the kernels attend with q, k rounded to bf16 (R11)
+    slack = fp32_lse_slack(pack, qn, kn) if dtype == torch.float32 else 0.0
+    assert lse_excess(l_c, L_ref, slack) <= 0, np.abs(l_c - L_ref).max()
+    print(f"  max|dO| {np.abs(o_c - O_ref).max():.3e}  max|dLSE| {np.abs(l_c - L_ref).max():.3e}", flush=True)
     if not check_bwd:
         return
     dq, dk, dv = _poisoned_like(qg), _poisoned_like(kg), _poisoned_like(vg)
     pp.pp_attn_bwd(pack, qg, kg, vg, o, lse, dog, dq=dq, dk=dk, dv=dv)
     dq_r, dk_r, dv_r = orc.attn_bwd(*args, qn, kn, vn, don)
+    out = {}
     for name, got, ref in (("dq", dq, dq_r), ("dk", dk, dk_r), ("dv", dv, dv_r)):
         g = got.double().cpu().numpy()
+        out[name] = (g, ref)
         assert np.isfinite(g).all(), f"unwritten {name}"
         if name in grads:
-            err = _rel_fro(g, ref)
-            assert err <= G_TOL, (name, err)
+            worst = check_grad(pack, name, g, ref)
+            print(f"  {name}: worst whole/segment rel. Frobenius {worst:.3e}", flush=True)
     # padding rows are exactly zero
     seg = orc.pack_segment_ids(*args)
     pad = seg < 0
@@ -79,6 +79,7 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
         assert (dq.cpu().double().numpy()[pad] == 0).all()
         assert (dk.cpu().double().numpy()[pad] == 0).all()
         assert (dv.cpu().double().numpy()[pad] == 0).all()
+    return out
 
 
 def test_tiny_fp32_config():
@@ -155,13 +156,17 @@ def test_scores_rising_along_the_row():
     """Every query's score grows by 0.2 per key position (plus small noise), so
     the running maximum rises by more than the rescale slack on every key tile
     and the softmax mass sits on each query's latest visible keys: the rescale
-    branch runs on nearly every tile of the forward.  O, LSE, dV and dK are
-    checked.  dQ is not: here dQ_i = scale sum_j dS_ij k_j sums near-one-hot
-    dS_ij (whose row sums are exactly 0) against keys that share one component
-    of size up to ~1000, so the bf16 rounding of dS (2^-9 relative per element,
-    as in any bf16 flash backward) is amplified by that component over its
-    spread inside the softmax window -- an ill-conditioned sum the gradient
-    tolerance does not cover.  dQ is checked by every other case."""
+    branch runs on nearly every tile of the forward.
+
+    O, LSE, dK and dV are held to the usual bars.  dQ is split by component.
+    Components 1..d-1 are held to the usual bar.  Component 0 is the one every
+    key shares with a value of up to ~1000: dQ_i0 = scale sum_j dS_ij k_j0 sums
+    near-one-hot dS_ij (whose row sums are exactly 0) against those large k_j0,
+    so the rounding of dS (2^-9 relative when it is rounded to bf16 for the
+    MFMA, plus P times the 2^-9 rounding of O inside delta) is amplified far
+    past a relative bar on the small result.  That component is held, element
+    by element, to twice the bound this rounding gives:
+        |err_i0| <= 2 scale sum_j 2^-9 (|dS_ij| + P_ij sum_c |dO_ic O_ic|) |k_j0|."""
     pack = wl.make_pack([300, 200], [[100, 130], [64, 97, 40]], pad=[0, 7])
     hq, hkv, d = 4, 2, 128
     q, k, v, do = _inputs(pack, hq, hkv, d, torch.bfloat16, 62)
@@ -177,7 +182,27 @@ def test_scores_rising_along_the_row():
     kf[:, :, 0] = (0.2 / scale) * pos[:, None]
     q, k = qf.to(torch.bfloat16), kf.to(torch.bfloat16)
     v = (v.float() * 0.5).to(torch.bfloat16)
-    _check_attention(pack, hq, hkv, d, torch.bfloat16, 62, inputs=(q, k, v, do), grads=("dk", "dv"))
+    res = _check_attention(pack, hq, hkv, d, torch.bfloat16, 62, inputs=(q, k, v, do), grads=("dk", "dv"))
+    dq_g, dq_r = res["dq"]
+    check_grad(pack, "dq[..., 1:]", dq_g[..., 1:], dq_r[..., 1:])
+    args = pack.oracle_args()
+    qn, kn, vn, don = (x.double().numpy() for x in (q, k, v, do))
+    O, _ = orc.attn_fwd(*args, qn, kn, vn)
+    G = hq // hkv
+    worst = 0.0
+    for b in range(pack.num_rows):
+        r0, r1 = int(rs[b]), int(rs[b + 1])
+        for h in range(hq):
+            Pm, M = orc.attn_probs(*args, qn, kn, b, h)
+            Vg, Kg = vn[r0:r1, h // G], kn[r0:r1, h // G]
+            dOh, Oh = don[r0:r1, h], O[r0:r1, h]
+            dS = Pm * (dOh @ Vg.T - (dOh * Oh).sum(axis=1)[:, None])
+            rnd = 2.0 ** -9 * (np.abs(dS) + Pm * np.abs(dOh * Oh).sum(axis=1)[:, None])
+            bound = 2 * scale * rnd @ np.abs(Kg[:, 0])
+            err = np.abs(dq_g[r0:r1, h, 0] - dq_r[r0:r1, h, 0])
+            assert (err <= bound + 1e-6).all(), (b, h, float((err - bound).max()))
+            worst = max(worst, float((err / (bound + 1e-6)).max()))
+    print(f"  dq[..., 0]: worst error / rounding bound {worst:.3f}", flush=True)
 
 
 def test_g8_long_prefix_small():

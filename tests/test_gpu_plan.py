@@ -4,8 +4,8 @@ The planned calls run the same kernels on the same metadata as the
 self-contained entry points, so their outputs must be bit-identical to
 pp_attn_fwd / pp_attn_bwd (and the rotary variants) for the same inputs; one
 case is also checked against the oracle directly, at the attention tolerances
-(O max-abs <= 1e-2 beyond its bf16 rounding, LSE max-abs <= 1e-2; dQ, dK, dV relative
-Frobenius <= 2e-2).  A plan is
+(O max-abs <= 1e-2 beyond its bf16 rounding, LSE within 2e-4 + 2^-16 |LSE|; dQ, dK, dV
+relative Frobenius <= 2e-2 on the whole tensor and on every prompt and response).  A plan is
 reused for several "layers" (different q, k, v) and does not depend on the
 caller's descriptor arrays after creation.
 """
@@ -16,7 +16,8 @@ import torch
 from oracle import pp_oracle as orc
 from paper_2602_24082_amd import binding as pp
 from paper_2602_24082_amd import workload as wl
-from tolerances import o_excess
+from gradcheck import check_grad
+from tolerances import lse_excess, o_excess
 
 pytestmark = pytest.mark.gpu
 
@@ -62,11 +63,11 @@ def test_planned_matches_oracle():
     qn, kn, vn, don = (x.double().numpy() for x in (q, k, v, do))
     O, L = orc.attn_fwd(*args, qn, kn, vn)
     assert o_excess(o.double().cpu().numpy(), O, True) <= 0
-    assert np.abs(lse.double().cpu().numpy() - L).max() <= 1e-2
-    for got, ref in zip((dq, dk, dv), orc.attn_bwd(*args, qn, kn, vn, don)):
+    assert lse_excess(lse.double().cpu().numpy(), L) <= 0
+    for name, got, ref in zip(("dq", "dk", "dv"), (dq, dk, dv), orc.attn_bwd(*args, qn, kn, vn, don)):
         g = got.double().cpu().numpy()
         assert np.isfinite(g).all()
-        assert np.linalg.norm(g - ref) / np.linalg.norm(ref) <= 2e-2
+        check_grad(pack, name, g, ref)
 
 
 def test_rotary_plan_equals_rotary_entry_points():

@@ -54,3 +54,76 @@ def test_bf16_arithmetic_needs_the_rounding_allowance():
     worst = np.abs(emul - O).max()
     assert worst > O_BAR                   # a flat 1e-2 fails the prescribed arithmetic
     assert o_excess(emul, O, True) <= 0    # the bar of R21 holds
+
+
+def test_fp32_lse_within_the_lse_bar():
+    """The LSE bar (tolerances.py) holds for log-sum-exp computed in fp32 from the
+    bf16 inputs -- scores summed in fp32, the exponentials in fp32 and summed in
+    fp32 in key order -- on a seeded pack with an 1100-token row, and is not so
+    loose that an error of one part in 1e3 would pass."""
+    from tolerances import lse_excess
+    pack = wl.make_pack([900, 60], [[150, 64], [33, 40, 17]])
+    hq, hkv, d = 4, 2, 128
+    G = hq // hkv
+    q, k, _, _ = wl.qkv(pack, hq, hkv, d, 2077, torch.bfloat16, device="cpu")
+    args = pack.oracle_args()
+    qn, kn = q.double().numpy(), k.double().numpy()
+    _, L = orc.attn_fwd(*args, qn, kn, kn)
+    q32, k32 = q.float().numpy(), k.float().numpy()
+    emul = np.zeros_like(L)
+    tau = np.float32(1.0 / np.sqrt(d))
+    for b in range(pack.num_rows):
+        r0, T = int(pack.row_start[b]), int(pack.row_start[b + 1] - pack.row_start[b])
+        K = int(pack.num_resp[b])
+        M = orc.row_mask(T, int(pack.prompt_len[b]), pack.resp_off[b, :K], pack.resp_len[b, :K])
+        for h in range(hq):
+            S = (q32[r0:r0 + T, h] @ k32[r0:r0 + T, h // G].T) * tau
+            S = np.where(M, S, np.float32(-np.inf)).astype(np.float32)
+            m = S.max(axis=1)
+            E = np.exp(S - m[:, None]).astype(np.float32)
+            l = np.cumsum(E, axis=1, dtype=np.float32)[:, -1]
+            emul[h, r0:r0 + T] = (m + np.log(l)).astype(np.float32)
+    assert lse_excess(emul, L) <= 0
+    assert lse_excess(L + 1e-3 * np.abs(L).max(), L) > 0
+
+
+def test_rope_lse_slack_covers_rounding_flips():
+    """Attention on the bf16 rounding of a rotation that is off by up to `err`
+    (as an fp32 rotation is) against attention on the rounding of the exact
+    rotation: the LSE difference exceeds the plain bar and stays inside the bar
+    widened by rope_lse_slack."""
+    from tolerances import bf16_rounding_ambiguity, lse_excess, rope_lse_slack
+    pack = wl.make_pack([300, 77], [[100, 28, 60], [64, 64]], pad=[0, 5])
+    hq, hkv, d, base = 4, 2, 64, 500000.0
+    q, k, _, _ = wl.qkv(pack, hq, hkv, d, 4040, torch.bfloat16, device="cpu")
+    args = pack.oracle_args()
+    qr = orc.pack_rope(*args, q.double().numpy(), base)
+    kr = orc.pack_rope(*args, k.double().numpy(), base)
+    eq, ek = 4e-6 * np.abs(qr).max(), 4e-6 * np.abs(kr).max()
+    rng = np.random.default_rng(9)
+    qp = qr + rng.uniform(-eq, eq, qr.shape)
+    kp = kr + rng.uniform(-ek, ek, kr.shape)
+    to_bf = lambda a: torch.from_numpy(a).to(torch.bfloat16).double().numpy()
+    assert (to_bf(qp) != to_bf(qr)).any() and (to_bf(kp) != to_bf(kr)).any()
+    assert bf16_rounding_ambiguity(qr, eq).any()
+    _, L_exact = orc.attn_fwd(*args, to_bf(qr), to_bf(kr), to_bf(kr))
+    _, L_pert = orc.attn_fwd(*args, to_bf(qp), to_bf(kp), to_bf(kr))
+    slack = rope_lse_slack(pack, qr, kr, eq, ek)
+    assert lse_excess(L_pert, L_exact) > 0          # the flips do exceed the plain bar
+    assert lse_excess(L_pert, L_exact, slack) <= 0  # and the slack covers them
+
+
+def test_fp32_lse_slack_covers_input_rounding():
+    """fp32 q, k rounded to bf16 (as the kernels do for fp32 callers): the LSE
+    change exceeds the plain bar on the tiny fp32 workload and stays inside the
+    bar widened by fp32_lse_slack."""
+    from tolerances import fp32_lse_slack, lse_excess
+    cfg = wl.CONFIGS[0]
+    pack = wl.config_pack(cfg)
+    q, k, _, _ = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, 11, torch.float32, device="cpu")
+    args = pack.oracle_args()
+    qn, kn = q.double().numpy(), k.double().numpy()
+    _, L = orc.attn_fwd(*args, qn, kn, kn)
+    _, L_b = orc.attn_fwd(*args, _bf16(qn), _bf16(kn), kn)
+    assert lse_excess(L_b, L) > 0
+    assert lse_excess(L_b, L, fp32_lse_slack(pack, qn, kn)) <= 0
