@@ -143,6 +143,27 @@ pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
                       const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
                       size_t ws_bytes, void* hip_stream);
 
+/* pp_attn_fwd for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation.  Same
+ * kernels, same plan and bit-identical results as pp_attn_fwd with dtype
+ * PP_BF16 (q, k, v, o are bf16; fp32 inputs would need workspace room for their
+ * bf16 copies and are not offered here), but no workspace argument: the plan's
+ * metadata is copied (hipMemcpyAsync from host memory, on hip_stream) into a
+ * static device array of PP_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every device it runs on until the process ends.  The call allocates no
+ * device memory and no pinned host memory (host-side planning uses ordinary
+ * heap memory).  Every call on a device reuses that device's array, whose
+ * contents are those of the last call: calls that overlap on one device (other
+ * streams, or unordered host threads) race; calls ordered on one stream do not.
+ * Errors as pp_attn_fwd; PP_ERR_WORKSPACE_TOO_SMALL when the pack's plan needs
+ * more than PP_NOALLOC_SCRATCH_BYTES (pp_workspace_size's fwd for PP_BF16 is
+ * the amount; about 4 bytes per token twice plus the tile lists, so roughly up
+ * to 400K tokens), before anything is enqueued. */
+#define PP_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+pp_status pp_attn_fwd_noalloc(const pp_pack_desc* desc, int hq, int hkv, int head_dim, float scale,
+                              const void* q, const void* k, const void* v, void* o, float* lse,
+                              void* hip_stream);
+
 /* Rotary position embedding on the packed position IDs.  Sec. 3.2 requires that
  * every packed token keep the position it has in its unpacked sequence: prompt
  * token t has position t, token j of a response has P_b + j (so every response

@@ -33,7 +33,10 @@ EXPORTED = [
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
     "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
     "pp_plan_workspace_size", "pp_plan_create", "pp_plan_destroy", "pp_attn_fwd_planned", "pp_attn_bwd_planned",
+    "pp_attn_fwd_noalloc",
 ]
+
+NOALLOC_SCRATCH_BYTES = 4 << 20  # PP_NOALLOC_SCRATCH_BYTES
 
 
 class PackStats(ctypes.Structure):
@@ -84,6 +87,7 @@ def lib() -> ctypes.CDLL:
                                     ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.pp_attn_fwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, sz, P]
     L.pp_attn_bwd.argtypes = [D, i, i, i, i, ctypes.c_float, P, P, P, P, P, P, P, P, P, P, sz, P]
+    L.pp_attn_fwd_noalloc.argtypes = [D, i, i, i, ctypes.c_float, P, P, P, P, P, P]
     f32 = ctypes.c_float
     L.pp_rope_workspace_size.argtypes = [D, i, ctypes.POINTER(sz)]
     L.pp_rope.argtypes = [D, i, i, i, f32, i, P, P, P, sz, P]
@@ -233,6 +237,23 @@ def pp_rope(pack: Pack, x: torch.Tensor, rope_base: float, inverse: bool = False
     _check(lib().pp_rope(h.ref, _dtype_code(x), H, d, float(rope_base), int(bool(inverse)), _ptr(x), _ptr(out),
                          _ptr(ws), ws.numel(), _stream(x.device)))
     return out
+
+
+def pp_attn_fwd_noalloc(pack: Pack, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, scale: float = 0.0,
+                        out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None):
+    """pp_attn_fwd (bf16) with the plan in the library's static device scratch
+    instead of a workspace; returns (o, lse).  Allocates o and lse here only
+    when they are not given."""
+    T, hq, d = q.shape
+    hkv = k.shape[1]
+    h = _DescHolder(pack)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty(hq, T, dtype=torch.float32, device=q.device)
+    _check(lib().pp_attn_fwd_noalloc(h.ref, hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                     _ptr(lse), _stream(q.device)))
+    return out, lse
 
 
 def pp_attn_fwd_rope(pack: Pack, q, k, v, rope_base: float, scale: float = 0.0, want_q_rot: bool = True,

@@ -23,7 +23,8 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 BUILD_DIR = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["pp_host.cpp", "pp_attn_fwd.hip", "pp_attn_bwd.hip", "pp_logprob.hip", "pp_rm.hip", "pp_rope.hip", "pp_stage.hip"]
+SOURCES = ["pp_host.cpp", "pp_attn_fwd.hip", "pp_attn_bwd.hip", "pp_logprob.hip", "pp_rm.hip", "pp_rope.hip", "pp_stage.hip",
+           "pp_noalloc.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -754,6 +754,18 @@ void drain_timing_locked() {
 
 }  // namespace
 
+pp_status report_error(pp_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+pp_status report_hip_error(hipError_t e, const char* what) { return hip_fail(e, what); }
+
 TimingScope::TimingScope(const char* name, hipStream_t stream) : slot_(-1), stream_(stream) {
   if (!g_time_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lk(g_time_mu);
@@ -976,6 +988,35 @@ pp_status attn_fwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
   return fwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, rope, s);
 }
+
+}  // namespace
+
+pp_status attn_fwd_fixed_scratch(const pp_pack_desc* desc, int hq, int hkv, int head_dim, float scale,
+                                 const void* q, const void* k, const void* v, void* o, float* lse,
+                                 size_t scratch_cap, pp_status (*get_scratch)(void** ptr), hipStream_t s) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if ((st = check_heads(hq, hkv, head_dim)) != PP_OK) return st;
+  if ((st = check_fwd_ptrs(bt.sumT, q, k, v, o, lse, nullptr)) != PP_OK) return st;
+  FwdPlan p;
+  plan_fwd(bt, PP_BF16, hq, hkv, head_dim, &p);
+  if (p.lay.total > scratch_cap)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL,
+                "this pack's forward plan needs %zu bytes of scratch; the library's static scratch holds %zu "
+                "(use pp_attn_fwd with a workspace)", p.lay.total, scratch_cap);
+  if (bt.sumT == 0) return PP_OK;
+  void* ws = nullptr;
+  if ((st = get_scratch(&ws)) != PP_OK) return st;
+  MetaImage img;
+  fwd_image(bt, p, head_dim, nullptr, &img);
+  // pageable host source: the runtime stages it itself, so nothing is allocated here
+  const hipError_t e = hipMemcpyAsync(ws, img.buf.data(), img.buf.size(), hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(plan into static scratch)");
+  return fwd_launch(p, ws, bt.sumT, PP_BF16, hq, hkv, head_dim, scale, q, k, v, o, lse, nullptr, s);
+}
+
+namespace {
 
 // The backward's metadata prefix as one host image.
 void bwd_image(const Batch& bt, const BwdPlan& p, int head_dim, const double* rope_base, MetaImage* out) {

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/pp_attn.h"
 #include "pp_plan.h"
 
 namespace pp {
@@ -185,5 +186,19 @@ struct LossLaunch {
   int32_t nr_inline[kLossInlineRows];  // K_b when B <= kLossInlineRows
 };
 hipError_t launch_loss(const LossLaunch& a, hipStream_t s);
+
+// Records `message` (printf-style) as the calling thread's pp_last_error and
+// returns st; the HIP variant appends the runtime's error string.
+pp_status report_error(pp_status st, const char* fmt, ...);
+pp_status report_hip_error(hipError_t e, const char* what);
+
+// pp_attn_fwd on bf16 q, k, v with the plan's metadata copied by hipMemcpyAsync
+// into a caller-provided device scratch of `scratch_cap` bytes instead of a
+// workspace; `get_scratch` is called after every argument has been validated
+// and the plan has been found to fit, and returns the scratch's device address.
+// Allocates no device memory and no pinned host memory.
+pp_status attn_fwd_fixed_scratch(const pp_pack_desc* desc, int hq, int hkv, int head_dim, float scale,
+                                 const void* q, const void* k, const void* v, void* o, float* lse,
+                                 size_t scratch_cap, pp_status (*get_scratch)(void** ptr), hipStream_t s);
 
 }  // namespace pp

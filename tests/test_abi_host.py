@@ -357,3 +357,25 @@ def test_misaligned_workspace_rejected():
     assert L.pp_plan_create(ctypes.byref(d), 0, 4, 2, 128, None, off, big, None, ctypes.byref(h)) == 1
     assert h.value is None
     assert b"256-byte" in L.pp_last_error()
+
+
+def test_noalloc_forward_rejects_packs_beyond_its_static_scratch():
+    """pp_attn_fwd_noalloc checks, before anything touches a GPU, that the pack's
+    plan fits the library's static scratch, and names the limit when it does
+    not (2000 rows of 300 tokens: 600K tokens of per-token metadata, > 4 MiB)."""
+    import torch
+    pack = wl.make_pack([200] * 2000, [[50, 50]] * 2000)
+    f, = binding.pp_workspace_size(pack, 8, 2, 128, fwd=True, bwd=False, loss=False)[:1]
+    assert f > binding.NOALLOC_SCRATCH_BYTES
+    h = binding._DescHolder(pack)
+    L = binding.lib()
+    dummy = ctypes.c_void_p(1 << 12)  # never dereferenced: the size check comes first
+    st = L.pp_attn_fwd_noalloc(h.ref, 8, 2, 128, 0.0, dummy, dummy, dummy, dummy, dummy, None)
+    assert st == 4  # PP_ERR_WORKSPACE_TOO_SMALL
+    msg = L.pp_last_error().decode()
+    assert str(binding.NOALLOC_SCRATCH_BYTES) in msg and str(f) in msg
+    # and bad arguments are still reported as such, not as a size problem
+    small = wl.make_pack([20], [[5, 5]])
+    hs = binding._DescHolder(small)
+    assert L.pp_attn_fwd_noalloc(hs.ref, 8, 3, 128, 0.0, dummy, dummy, dummy, dummy, dummy, None) == 1
+    assert L.pp_attn_fwd_noalloc(hs.ref, 8, 2, 96, 0.0, dummy, dummy, dummy, dummy, dummy, None) == 3
