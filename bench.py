@@ -25,7 +25,6 @@ kernels on the unpacked, prompt-duplicated, padded layout.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -50,18 +49,13 @@ ROPE_BASE = {32: 500000.0, 64: 1000000.0}  # rotary base by query-head count (Ll
 DPO_BETA = 0.1
 
 
-CSRC = os.path.join(ROOT, "paper_2602_24082_amd", "csrc")
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_dpo_step_llama3_8b_gqa32x8_d128.txt")
 
 
 def source_hash() -> str:
-    """sha256 over the HIP/C++ sources of the library (names and contents)."""
-    h = hashlib.sha256()
-    for fn in sorted(os.listdir(CSRC)):
-        h.update(fn.encode())
-        with open(os.path.join(CSRC, fn), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()
+    """sha256 over the library's sources (the build id embedded in the library)."""
+    from paper_2602_24082_amd.build import source_digest
+    return source_digest()
 
 
 def traffic_from_profile(kernel: str):

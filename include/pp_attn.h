@@ -84,12 +84,20 @@ typedef enum pp_status {
   PP_ERR_BAD_LAYOUT = 2,        /* descriptor violates the packed layout above */
   PP_ERR_UNSUPPORTED = 3,       /* valid but not implemented (e.g. head_dim)  */
   PP_ERR_WORKSPACE_TOO_SMALL = 4,
-  PP_ERR_HIP = 5                /* a HIP runtime call failed */
+  PP_ERR_HIP = 5,               /* a HIP runtime call failed */
+  /* range markers, not statuses: they make every int32 a valid value of the
+     type, so an out-of-range value from a caller is defined behaviour */
+  PP_STATUS_RANGE_MIN_ = -0x7fffffff - 1,
+  PP_STATUS_RANGE_MAX_ = 0x7fffffff
 } pp_status;
 
 typedef enum pp_dtype {
   PP_BF16 = 0,  /* bfloat16 */
-  PP_FP32 = 1   /* float; attention inputs are rounded to bf16 (nearest even) */
+  PP_FP32 = 1,  /* float; attention inputs are rounded to bf16 (nearest even) */
+  /* range markers (see pp_status): any other value is rejected with
+     PP_ERR_INVALID_ARGUMENT */
+  PP_DTYPE_RANGE_MIN_ = -0x7fffffff - 1,
+  PP_DTYPE_RANGE_MAX_ = 0x7fffffff
 } pp_dtype;
 
 /* Host description of a packed batch; see "The packed layout" above. */
@@ -396,6 +404,10 @@ const char* pp_status_string(pp_status status);
 const char* pp_last_error(void);
 /* ABI version: major * 10000 + minor * 100 + patch. */
 int pp_version(void);
+/* Identity of the sources this library was built from: the hex sha256 over the
+ * library's source files and this header (names and contents), fixed at build
+ * time, so a caller can tell a library built from other sources.  Static string. */
+const char* pp_build_id(void);
 
 #ifdef __cplusplus
 }

@@ -18,7 +18,8 @@ import torch
 from .workload import Pack
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libppattn.so")
+# PP_LIB_PATH selects another build of the library (e.g. a host-sanitized one)
+LIB_PATH = os.environ.get("PP_LIB_PATH") or os.path.join(_PKG, "libppattn.so")
 
 PP_OK = 0
 PP_BF16 = 0
@@ -33,7 +34,7 @@ EXPORTED = [
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
     "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
     "pp_plan_workspace_size", "pp_plan_create", "pp_plan_destroy", "pp_attn_fwd_planned", "pp_attn_bwd_planned",
-    "pp_attn_fwd_noalloc",
+    "pp_attn_fwd_noalloc", "pp_build_id",
 ]
 
 NOALLOC_SCRATCH_BYTES = 4 << 20  # PP_NOALLOC_SCRATCH_BYTES
@@ -78,6 +79,12 @@ def lib() -> ctypes.CDLL:
         raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_24082_amd.build` "
                           "(there is no non-HIP fallback)")
     L = ctypes.CDLL(LIB_PATH)
+    L.pp_build_id.restype = ctypes.c_char_p
+    from .build import source_digest
+    built, want = L.pp_build_id().decode(), source_digest()
+    if built != want:
+        raise ImportError(f"{LIB_PATH} was built from other sources (build id {built[:12]}, sources {want[:12]}): "
+                          "rebuild it with `python -m paper_2602_24082_amd.build`")
     P = ctypes.c_void_p
     i32 = ctypes.c_int32
     i = ctypes.c_int

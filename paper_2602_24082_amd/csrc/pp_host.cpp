@@ -736,8 +736,14 @@ hipEvent_t pool_get() {
 void drain_timing_locked() {
   for (auto& r : g_time_pending) {
     float ms = 0.f;
-    hipEventSynchronize(r.stop);
-    hipEventElapsedTime(&ms, r.start, r.stop);
+    // a launch whose events cannot be read (e.g. a failed record) is dropped,
+    // not counted as a zero-length launch
+    if (hipEventSynchronize(r.stop) != hipSuccess || hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+      (void)hipGetLastError();
+      g_event_pool.push_back(r.start);
+      g_event_pool.push_back(r.stop);
+      continue;
+    }
     bool found = false;
     for (auto& t : g_time_totals)
       if (strcmp(t.name, r.name) == 0) {
@@ -766,21 +772,31 @@ pp_status report_error(pp_status st, const char* fmt, ...) {
 
 pp_status report_hip_error(hipError_t e, const char* what) { return hip_fail(e, what); }
 
-TimingScope::TimingScope(const char* name, hipStream_t stream) : slot_(-1), stream_(stream) {
+TimingScope::TimingScope(const char* name, hipStream_t stream) : name_(name), stream_(stream) {
   if (!g_time_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lk(g_time_mu);
   if (!timing_selected_locked(name)) return;
   hipEvent_t a = pool_get(), b = pool_get();
-  if (!a || !b) return;
-  if (hipEventRecord(a, stream) != hipSuccess) return;
-  g_time_pending.push_back({name, a, b});
-  slot_ = (int)g_time_pending.size() - 1;
+  if (!a || !b || hipEventRecord(a, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    if (a) g_event_pool.push_back(a);
+    if (b) g_event_pool.push_back(b);
+    return;
+  }
+  start_ = a;
+  stop_ = b;
 }
 
 TimingScope::~TimingScope() {
-  if (slot_ < 0) return;
+  if (!start_) return;
   std::lock_guard<std::mutex> lk(g_time_mu);
-  if (slot_ < (int)g_time_pending.size()) hipEventRecord(g_time_pending[slot_].stop, stream_);
+  if (hipEventRecord(stop_, stream_) == hipSuccess) {
+    g_time_pending.push_back({name_, start_, stop_});
+  } else {
+    (void)hipGetLastError();
+    g_event_pool.push_back(start_);
+    g_event_pool.push_back(stop_);
+  }
 }
 
 }  // namespace pp
@@ -793,7 +809,12 @@ using namespace pp;
 
 extern "C" {
 
+#ifndef PP_BUILD_ID
+#define PP_BUILD_ID "unknown"
+#endif
 int pp_version(void) { return 100; }
+
+const char* pp_build_id(void) { return PP_BUILD_ID; }
 
 const char* pp_status_string(pp_status s) {
   switch (s) {
@@ -803,6 +824,7 @@ const char* pp_status_string(pp_status s) {
     case PP_ERR_UNSUPPORTED: return "unsupported";
     case PP_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
     case PP_ERR_HIP: return "HIP error";
+    default: break;
   }
   return "unknown status";
 }

@@ -14,14 +14,19 @@ namespace pp {
 enum ElemType { kBF16 = 0, kFP32 = 1 };
 
 // Brackets one kernel launch with hipEvents on its stream while timing is on.
+// The scope owns its two events until its destructor has recorded the second;
+// only then does the launch join the list that pp_timing_get drains, so a
+// drain from another thread never sees a half-recorded launch.
 struct TimingScope {
   TimingScope(const char* name, hipStream_t stream);
   ~TimingScope();
   TimingScope(const TimingScope&) = delete;
   TimingScope& operator=(const TimingScope&) = delete;
  private:
-  int slot_;
+  const char* name_;
   hipStream_t stream_;
+  hipEvent_t start_ = nullptr;
+  hipEvent_t stop_ = nullptr;
 };
 
 // Copies `bytes` from src (the device address of mapped pinned host memory) to
