@@ -198,12 +198,119 @@ def cpu_baseline(pack, cfg, rows, seed):
         orc.attn_bwd(*args, qn, kn, vn, don)
         secs += time.perf_counter() - t0
         flops += 14 * cfg.head_dim * cfg.hq * useful_pairs(one)
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    threads = max([i.get("num_threads", 1) for i in blas] + [1])
     return {"value": flops / secs / 1e12, "unit": "useful TFLOP/s (attention fwd+bwd)",
             "cores": int(threads), "kind": "oracle",
+            "cpu_model": cpu_model(), "usable_cores": len(os.sched_getaffinity(0)),
+            "blas_threads": int(threads),
+            "blas": ",".join(sorted({f'{i.get("internal_api", "?")} {i.get("version", "")}'.strip() for i in blas})),
             "sample": (f"rows {list(rows)} of the benchmarked batch (T={[int(pack.row_lengths()[b]) for b in rows]}), "
-                       f"all {cfg.hq} heads, attention fwd+bwd in fp64 numpy, {secs:.1f} s; "
-                       f"host has {len(os.sched_getaffinity(0))} usable cores")}
+                       f"all {cfg.hq} heads, attention fwd+bwd in fp64 numpy, {secs:.1f} s; 'cores' = the BLAS "
+                       f"threads the oracle's matrix products ran on (its elementwise work is single-threaded)")}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def attention_memory(pack, hq, hkv, d, dev):
+    """Device memory of one attention fwd+bwd on a layout: the allocator's
+    high-water mark above what was allocated before, with q, k, v, dO, the
+    outputs O and LSE, the gradients and both workspaces live (the library
+    allocates nothing itself: every byte is a caller tensor).  Returns
+    (peak bytes, of which activations q, k, v, O, LSE)."""
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    base = torch.cuda.memory_allocated(dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    a = Attn(pack, hq, hkv, d, 977, dev)
+    a.run()
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated(dev) - base
+    act = sum(t.numel() * t.element_size() for t in (a.q, a.k, a.v, a.o, a.lse))
+    del a
+    torch.cuda.empty_cache()
+    return int(peak), int(act)
+
+
+def memory_leg(pack, hq, hkv, d, dev):
+    """Measured attention memory of the packed layout against the unpacked
+    layouts (Sec. 3.2.1: with linear-memory attention, memory follows tokens),
+    next to the ratios the cost model predicts."""
+    st = pp.pp_pack_stats(pack)
+    out = {}
+    for name, lay in (("packed", pack), ("unpacked_varlen", wl.unpacked_varlen(pack)),
+                      ("unpacked_padded", wl.unpacked_padded(pack))):
+        peak, act = attention_memory(lay, hq, hkv, d, dev)
+        out[name] = {"tokens": lay.total_tokens, "peak_bytes": peak, "activation_bytes": act}
+    for name in ("unpacked_varlen", "unpacked_padded"):
+        out[f"packed_over_{name}_peak"] = round(out["packed"]["peak_bytes"] / out[name]["peak_bytes"], 4)
+        out[f"packed_over_{name}_activations"] = round(
+            out["packed"]["activation_bytes"] / out[name]["activation_bytes"], 4)
+    out["tokens_packed_over_unpacked"] = round(st["tokens_packed"] / st["tokens_unpacked"], 4)
+    out["eq1_memory_ratio"] = round(st["eq1_memory_ratio"], 4)
+    out["measured_by"] = ("torch.cuda.max_memory_allocated over one attention fwd+bwd (inputs, dO, O, LSE, "
+                          "gradients, workspaces)")
+    return out
+
+
+def attention_kernels(pack, hq, hkv, d, dev, iters=5):
+    """Per-kernel average launch times of attention fwd+bwd on a pack (library
+    events around every launch) and each kernel's fraction of the bf16 peak on
+    its useful work."""
+    a = Attn(pack, hq, hkv, d, 977, dev)
+    for _ in range(2):
+        a.run()
+    torch.cuda.synchronize()
+    pp.pp_timing_select(None)
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    for _ in range(iters):
+        a.run()
+    torch.cuda.synchronize()
+    pp.pp_timing_enable(False)
+    kt = pp.pp_timing_get()
+    del a
+    torch.cuda.empty_cache()
+    U = useful_pairs(pack)
+    per = {"pp_attn_fwd": 4, "pp_attn_bwd_dkdv": 8, "pp_attn_bwd_dq": 2}
+    out = {}
+    for k, units in per.items():
+        if k in kt:
+            ms = kt[k][0] / kt[k][1]
+            ach = units * d * hq * U / (ms * 1e-3) / 1e12
+            out[k] = {"avg_ms": round(ms, 4), "useful_TFLOP_s": round(ach, 1), "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
+    bwd_ms = sum(kt[k][0] / kt[k][1] for k in ("pp_attn_bwd_prep", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq") if k in kt)
+    if bwd_ms > 0:
+        ach = 10 * d * hq * U / (bwd_ms * 1e-3) / 1e12
+        out["backward_10_units"] = {"ms": round(bwd_ms, 4), "useful_TFLOP_s": round(ach, 1),
+                                    "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
+    return out
+
+
+def workload_leg(cfg_index, dev):
+    """Attention fwd+bwd of another workload: useful TFLOP/s of the whole pass
+    (HIP events around it, no per-launch events inside) and per kernel, and the
+    speedup over the same kernels on the unpacked padded layout."""
+    cfg = wl.CONFIGS[cfg_index]
+    pack = wl.config_pack(cfg)
+    hq, hkv, d = cfg.hq, cfg.hkv, cfg.head_dim
+    U = useful_pairs(pack)
+    t = time_attention(pack, hq, hkv, d, dev, iters=5, warmup=2)
+    t_pad = time_attention(wl.unpacked_padded(pack), hq, hkv, d, dev, iters=3, warmup=1)
+    tf = 14 * d * hq * U / (t * 1e-3) / 1e12
+    return {"workload": cfg.name, "rows": pack.num_rows, "tokens": pack.total_tokens, "useful_pairs": U,
+            "attn_fwd_bwd_ms": round(t, 4), "useful_TFLOP_s": round(tf, 1),
+            "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+            "unpacked_padded_ms": round(t_pad, 4), "speedup_vs_padded": round(t_pad / t, 3),
+            "kernels": attention_kernels(pack, hq, hkv, d, dev)}
 
 
 def chain_sorting(dev, reps=1):
@@ -288,9 +395,10 @@ def chain_sorting(dev, reps=1):
     for c in cells.values():
         c["one_gpu_speedup"] = round(base["one_gpu_ms"] / c["one_gpu_ms"], 3)
         c["simulated_dp8_speedup"] = round(base["simulated_dp8_ms"] / c["simulated_dp8_ms"], 3)
-    print(json.dumps({"metric": "DPO kernel chain with batch sorting (72B-shaped, 128 samples, 8 batches of 16)",
-                      "unit": "ms", "data": "synthetic", "dtype": "bf16",
-                      "config": {"workload": cfg.name, "vocab": V, "beta": cfg.beta}, "cells": cells}))
+    del logits, tokens
+    torch.cuda.empty_cache()
+    return {"metric": "DPO kernel chain with batch sorting (72B-shaped, 128 samples, 8 batches of 16)",
+            "unit": "ms", "workload": cfg.name, "vocab": V, "beta": cfg.beta, "cells": cells}
 
 
 def plan_leg(pack, cfg, seed, dev, layers=8):
@@ -406,7 +514,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
-    ap.add_argument("--chain-sorting", action="store_true")
+    ap.add_argument("--chain-sorting", action="store_true", help="print only the DPO chain leg")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the other workloads, the measured memory and the DPO chain")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the packed rows shard by "
@@ -420,7 +530,7 @@ def main():
         calib_copy(dev)
         return
     if args.chain_sorting:
-        chain_sorting(dev)
+        print(json.dumps(chain_sorting(dev)))
         return
 
     cfg = wl.CONFIGS[args.config]
@@ -466,10 +576,12 @@ def main():
     # algorithmic work per launch of each kernel (FLOPs of the GEMMs its algorithm
     # performs, or bytes it must move)
     n_rows = logit_rows_needed(pack)
+    # dQ's useful work is its own product, dQ = scale dS K (2 d Hq per pair);
+    # the S and dP it recomputes (4 d Hq per pair) are counted by dK/dV
     per_launch = {
         "pp_attn_fwd": ("mfma", 4 * d * hq * U),
         "pp_attn_bwd_dkdv": ("mfma", 8 * d * hq * U),
-        "pp_attn_bwd_dq": ("mfma", 6 * d * hq * U),
+        "pp_attn_bwd_dq": ("mfma", 2 * d * hq * U),
         "pp_logprob_rows": ("hbm", n_rows * V * 2 + n_rows * 16),
     }
 
@@ -529,6 +641,18 @@ def main():
             ach = per_launch[k][1] / (k_ms * 1e-3) / 1e12
             attn_roofs[k] = {"achieved_TFLOP_s": round(ach, 1), "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                              "avg_ms": round(k_ms, 4), "algorithmic_flops_per_launch": per_launch[k][1]}
+    if "pp_attn_bwd_dq" in attn_roofs:
+        # the recomputed S and dP, executed but not useful
+        k_ms = attn_roofs["pp_attn_bwd_dq"]["avg_ms"]
+        attn_roofs["pp_attn_bwd_dq"]["recompute_flops_per_launch"] = 4 * d * hq * U
+        attn_roofs["pp_attn_bwd_dq"]["executed_TFLOP_s"] = round(6 * d * hq * U / (k_ms * 1e-3) / 1e12, 1)
+    bwd_keys = ("pp_attn_bwd_prep", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq")
+    if all(k in kern_all for k in bwd_keys):
+        bwd_ms = sum(kern_all[k][0] / kern_all[k][1] for k in bwd_keys)
+        ach = 10 * d * hq * U / (bwd_ms * 1e-3) / 1e12
+        attn_roofs["backward_10_units"] = {"ms": round(bwd_ms, 4), "useful_TFLOP_s": round(ach, 1),
+                                           "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                                           "rule": "10 d Hq FLOPs per visible pair over delta + dK/dV + dQ"}
     lp = kern.get("pp_logprob_rows") or kern_all.get("pp_logprob_rows")
     logprob = None
     if lp:
@@ -562,6 +686,29 @@ def main():
                        "bytes_rule": "needed logit rows read once + every dlogits row written once (bf16)",
                        "traffic": traffic_from_profile("pp_logprob_bwd") if args.config == 1 else None}
     del dlogits
+    # the gathered form: only the predicting rows are written
+    n_g = pp.pp_logprob_row_count(pack)
+    d_rows = torch.empty(n_g, V, dtype=logits_pol.dtype, device=dev)
+    r_idx = torch.empty(n_g, dtype=torch.int32, device=dev)
+    for _ in range(2):
+        pp.pp_seq_logprob_bwd_rows(pack, logits_pol, tokens, dseq, dlogits_rows=d_rows, row_index=r_idx, ws=ws_lp)
+    torch.cuda.synchronize()
+    pp.pp_timing_reset()
+    pp.pp_timing_enable(True)
+    for _ in range(max(3, args.steps // 2)):
+        pp.pp_seq_logprob_bwd_rows(pack, logits_pol, tokens, dseq, dlogits_rows=d_rows, row_index=r_idx, ws=ws_lp)
+    torch.cuda.synchronize()
+    pp.pp_timing_enable(False)
+    kg = pp.pp_timing_get().get("pp_logprob_bwd_rows")
+    if kg and logprob_bwd is not None:
+        kg_ms = kg[0] / kg[1]
+        nbytes = 2 * n_g * V * 2 + n_g * 4
+        gbs = nbytes / (kg_ms * 1e-3) / 1e9
+        logprob_bwd["gathered_rows"] = {"kernel": "pp_logprob_bwd_rows", "rows": n_g, "GB_per_s": round(gbs, 1),
+                                        "frac_hbm": round(gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": nbytes,
+                                        "avg_ms": round(kg_ms, 4),
+                                        "bytes_rule": "each predicting row read once and written once (bf16)"}
+    del d_rows, r_idx
 
     # reward-model head (scores on each response's last hidden state, then its
     # backward) on the same pack, hidden size of the named model
@@ -597,6 +744,15 @@ def main():
         losing = {"workload": "8 rows, prompt 32-96, K=2 responses 768-1024 (responses >> prompt)",
                   **losing[0], **losing[1]}
 
+    memory = workloads = chain = None
+    if not args.no_extra:
+        # free the step's large buffers first: the other legs allocate their own
+        del logits_pol, logits_ref, attn
+        torch.cuda.empty_cache()
+        memory = memory_leg(pack, hq, cfg.hkv, d, dev)
+        workloads = {wl.CONFIGS[i].name: workload_leg(i, dev) for i in (2, 3, 4) if i != args.config}
+        chain = chain_sorting(dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(pack, cfg, list(range(pack.num_rows)), seed)
@@ -629,6 +785,9 @@ def main():
         "rm_head": rm_head,
         "rope": rope,
         "plan": plan,
+        "memory": memory,
+        "workloads": workloads,
+        "dpo_chain_sorting": chain,
         "kernels": kernels,
         "kernel_breakdown_steps": n_breakdown,
         "attention_rooflines": attn_roofs,

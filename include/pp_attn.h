@@ -11,7 +11,8 @@
  *   pp_attn_fwd     masked attention forward over packed rows  (Sec. 3.2)
  *   pp_attn_bwd     its gradients dQ, dK, dV                   (Sec. 3.2)
  *   pp_seq_logprob  per-response summed token log-probs        (Sec. 2.1, Sec. 3.2)
- *   pp_seq_logprob_bwd  their gradient with respect to the logits
+ *   pp_seq_logprob_bwd  their gradient with respect to the logits (all rows,
+ *                   or only the rows that predict a response token)
  *   pp_rm_scores    reward-model head on each response's last token (Sec. 2.1)
  *   pp_rm_scores_bwd    its gradients
  *   pp_dpo_loss     ranked-pair DPO / Bradley-Terry loss        (Sec. 2.1)
@@ -301,6 +302,24 @@ pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vo
 pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
                              const void* logits, const int32_t* tokens, const float* dseq,
                              void* dlogits, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* pp_seq_logprob_bwd restricted to the logit rows that predict a response token
+ * (Sec. 2.1 scores over the Sec. 3.2 layout): only those rows -- a row's last
+ * prompt position once (it predicts the first token of every response), then
+ * for each response k its positions o_bk .. o_bk + L_bk - 2 -- are written,
+ * back to back in that order (rows of the batch in order), so the gradient of a
+ * batch costs one read and one write of each such row instead of a write of all
+ * sumT rows.  pp_logprob_row_count gives their number n (host only).
+ * dlogits_rows: dev [n, vocab] in logits_dtype; row i is the gradient of the
+ * flat logit row row_index[i] (dev int32 [n], strictly increasing, may be NULL)
+ * and equals that row of pp_seq_logprob_bwd's output bit for bit; every other
+ * row of the dense gradient is 0.  Arguments and errors as pp_seq_logprob_bwd
+ * (ws_bytes >= pp_workspace_size's logprob). */
+pp_status pp_logprob_row_count(const pp_pack_desc* desc, int64_t* n_rows);
+pp_status pp_seq_logprob_bwd_rows(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                                  const void* logits, const int32_t* tokens, const float* dseq,
+                                  void* dlogits_rows, int32_t* row_index, void* ws, size_t ws_bytes,
+                                  void* hip_stream);
 
 /* Reward-model head (Sec. 2.1: the reward model maps a token sequence to a
  * scalar).  The score of the sequence (prompt b, response k) is

@@ -488,6 +488,21 @@ def logprob_rows_needed(prompt_len, num_resp, resp_len):
     return n
 
 
+def logprob_predicting_rows(row_start, prompt_len, num_resp, resp_off, resp_len):
+    """Flat logit rows that predict at least one response token, ascending
+    (Sec. 3.2 packed layout, R8): token j of response k of row b is predicted by
+    the row's last prompt position when j = 0 and by the position before it
+    otherwise."""
+    rows = set()
+    for b in range(len(prompt_len)):
+        r0, P = int(row_start[b]), int(prompt_len[b])
+        for k in range(int(num_resp[b])):
+            o, L = int(resp_off[b][k]), int(resp_len[b][k])
+            for j in range(L):
+                rows.add(r0 + (P - 1 if j == 0 else o + j - 1))
+    return sorted(rows)
+
+
 # ----------------------------------------------------------------------------
 # Bradley-Terry / DPO loss over ranked pairs (Sec. 2.1, R3-R6, R10)
 # ----------------------------------------------------------------------------

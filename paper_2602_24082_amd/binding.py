@@ -34,7 +34,7 @@ EXPORTED = [
     "pp_timing_count", "pp_timing_get", "pp_status_string", "pp_last_error", "pp_version",
     "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
     "pp_plan_workspace_size", "pp_plan_create", "pp_plan_destroy", "pp_attn_fwd_planned", "pp_attn_bwd_planned",
-    "pp_attn_fwd_noalloc", "pp_build_id",
+    "pp_attn_fwd_noalloc", "pp_build_id", "pp_logprob_row_count", "pp_seq_logprob_bwd_rows",
 ]
 
 NOALLOC_SCRATCH_BYTES = 4 << 20  # PP_NOALLOC_SCRATCH_BYTES
@@ -107,6 +107,8 @@ def lib() -> ctypes.CDLL:
     L.pp_attn_bwd_planned.argtypes = [P, f32, P, P, P, P, P, P, P, P, P, P]
     L.pp_seq_logprob.argtypes = [D, i, i, P, P, P, P, P, sz, P]
     L.pp_seq_logprob_bwd.argtypes = [D, i, i, P, P, P, P, P, sz, P]
+    L.pp_logprob_row_count.argtypes = [D, ctypes.POINTER(ctypes.c_int64)]
+    L.pp_seq_logprob_bwd_rows.argtypes = [D, i, i, P, P, P, P, P, P, sz, P]
     L.pp_rm_workspace_size.argtypes = [D, ctypes.POINTER(sz)]
     L.pp_pack_stats.argtypes = [D, ctypes.POINTER(PackStats)]
     L.pp_rm_scores.argtypes = [D, i, i, P, P, ctypes.c_float, P, P, sz, P]
@@ -407,6 +409,38 @@ def pp_seq_logprob_bwd(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, d
     _check(lib().pp_seq_logprob_bwd(h.ref, _dtype_code(logits), V, _ptr(logits), _ptr(tokens), _ptr(dseq),
                                     _ptr(dlogits), _ptr(ws), ws.numel(), _stream(dev)))
     return dlogits
+
+
+def pp_logprob_row_count(pack: Pack) -> int:
+    """Number of logit rows that predict a response token."""
+    h = _DescHolder(pack)
+    n = ctypes.c_int64(0)
+    _check(lib().pp_logprob_row_count(h.ref, ctypes.byref(n)))
+    return int(n.value)
+
+
+def pp_seq_logprob_bwd_rows(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, dseq: torch.Tensor,
+                            dlogits_rows=None, row_index=None, ws=None):
+    """Gradient of sum(dseq * seq_logp) on the predicting logit rows only:
+    (dlogits_rows [n, V] in the logits' dtype, row_index [n] int32)."""
+    V = logits.shape[1]
+    h = _DescHolder(pack)
+    dev = logits.device
+    n = pp_logprob_row_count(pack)
+    if dlogits_rows is None:
+        dlogits_rows = torch.empty(n, V, dtype=logits.dtype, device=dev)
+    if row_index is None:
+        row_index = torch.empty(n, dtype=torch.int32, device=dev)
+    if ws is None:
+        nb = pp_workspace_size(pack, vocab=V, fwd=False, bwd=False, logprob=True, loss=False)[2]
+        ws = _workspace(nb, dev)
+    if tokens.dtype != torch.int32:
+        raise TypeError("tokens must be int32")
+    if dseq.dtype != torch.float32 or not dseq.is_contiguous():
+        raise TypeError("dseq must be contiguous float32 [B, K_max]")
+    _check(lib().pp_seq_logprob_bwd_rows(h.ref, _dtype_code(logits), V, _ptr(logits), _ptr(tokens), _ptr(dseq),
+                                         _ptr(dlogits_rows), _ptr(row_index), _ptr(ws), ws.numel(), _stream(dev)))
+    return dlogits_rows, row_index
 
 
 def pp_rm_workspace_size(pack: Pack) -> int:

@@ -1419,9 +1419,16 @@ pp_status pp_seq_logprob(const pp_pack_desc* desc, pp_dtype logits_dtype, int vo
   return PP_OK;
 }
 
-pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
-                             const void* logits, const int32_t* tokens, const float* dseq,
-                             void* dlogits, void* ws, size_t ws_bytes, void* hip_stream) {
+}  // extern "C"
+
+namespace pp {
+namespace {
+
+// The log-prob backward, dense (dlogits [sumT, vocab]) or gathered (one row per
+// logit row that predicts a response token, [n, vocab], and row_index [n]).
+pp_status logprob_bwd_impl(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab, const void* logits,
+                           const int32_t* tokens, const float* dseq, void* dlogits, bool gathered,
+                           int32_t* row_index, void* ws, size_t ws_bytes, void* hip_stream) {
   Batch bt;
   pp_status st = read_desc(desc, &bt);
   if (st != PP_OK) return st;
@@ -1432,10 +1439,11 @@ pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, in
     return fail(PP_ERR_UNSUPPORTED, "the log-prob backward takes at most %d responses per row (max_resp %d)",
                 kMaxRowLabels, bt.Kmax);
   if (bt.sumT == 0) return PP_OK;
-  if (!logits || !tokens || !dlogits) return fail(PP_ERR_INVALID_ARGUMENT, "logits, tokens and dlogits must be non-NULL");
-  if (bt.Kmax > 0 && !dseq) return fail(PP_ERR_INVALID_ARGUMENT, "dseq is NULL");
   LogprobPlan p;
   plan_logprob(bt, &p);
+  if (gathered && p.l.rows.empty()) return PP_OK;
+  if (!logits || !tokens || !dlogits) return fail(PP_ERR_INVALID_ARGUMENT, "logits, tokens and dlogits must be non-NULL");
+  if (bt.Kmax > 0 && !dseq) return fail(PP_ERR_INVALID_ARGUMENT, "dseq is NULL");
   if (ws_bytes < p.lay.total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL, "logprob needs %zu workspace bytes, got %zu", p.lay.total,
                 ws_bytes);
@@ -1447,7 +1455,7 @@ pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, in
   img.put(p.lay.regions[p.r_labels], p.l.labels.data(), p.l.labels.size() * 4);
   img.put(p.lay.regions[p.r_resp], p.l.resp.data(), p.l.resp.size() * sizeof(RespItem));
   img.put(p.lay.regions[p.r_label_out], p.l.label_out.data(), p.l.label_out.size() * 4);
-  img.put(p.lay.regions[p.r_row_item], p.row_item.data(), p.row_item.size() * 4);
+  if (!gathered) img.put(p.lay.regions[p.r_row_item], p.row_item.data(), p.row_item.size() * 4);
   if ((st = stage_copy(ws, img.buf.data(), img.buf.size(), s)) != PP_OK) return st;
   LogprobBwdLaunch a{};
   a.logits = logits;
@@ -1461,9 +1469,44 @@ pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, in
   a.vocab = vocab;
   a.sumT = bt.sumT;
   a.dtype = logits_dtype == PP_FP32 ? kFP32 : kBF16;
+  a.gathered = gathered;
+  a.n_rows = (int)p.l.rows.size();
+  a.row_index = row_index;
   hipError_t e = launch_logprob_bwd(a, s);
   if (e != hipSuccess) return hip_fail(e, "logprob backward launch");
   return PP_OK;
+}
+
+}  // namespace
+}  // namespace pp
+
+extern "C" {
+
+pp_status pp_seq_logprob_bwd(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                             const void* logits, const int32_t* tokens, const float* dseq,
+                             void* dlogits, void* ws, size_t ws_bytes, void* hip_stream) {
+  return logprob_bwd_impl(desc, logits_dtype, vocab, logits, tokens, dseq, dlogits, false, nullptr, ws, ws_bytes,
+                          hip_stream);
+}
+
+pp_status pp_logprob_row_count(const pp_pack_desc* desc, int64_t* n_rows) {
+  Batch bt;
+  pp_status st = read_desc(desc, &bt);
+  if (st != PP_OK) return st;
+  if (!n_rows) return fail(PP_ERR_INVALID_ARGUMENT, "n_rows is NULL");
+  if ((st = check_logprob_layout(bt)) != PP_OK) return st;
+  LPlan l;
+  build_lplan(bt, &l);
+  *n_rows = (int64_t)l.rows.size();
+  return PP_OK;
+}
+
+pp_status pp_seq_logprob_bwd_rows(const pp_pack_desc* desc, pp_dtype logits_dtype, int vocab,
+                                  const void* logits, const int32_t* tokens, const float* dseq,
+                                  void* dlogits_rows, int32_t* row_index, void* ws, size_t ws_bytes,
+                                  void* hip_stream) {
+  return logprob_bwd_impl(desc, logits_dtype, vocab, logits, tokens, dseq, dlogits_rows, true, row_index, ws,
+                          ws_bytes, hip_stream);
 }
 
 pp_status pp_rm_workspace_size(const pp_pack_desc* desc, size_t* bytes) {

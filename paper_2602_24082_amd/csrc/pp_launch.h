@@ -142,6 +142,11 @@ struct LogprobBwdLaunch {
   int vocab;
   int sumT;
   int dtype;
+  // gathered mode: one output row per gather record (dlogits is [n_rows, vocab]),
+  // in record order, and the flat logit row of each into row_index (may be null)
+  bool gathered = false;
+  int n_rows = 0;
+  int32_t* row_index = nullptr;
 };
 hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s);
 

@@ -216,16 +216,21 @@ struct Pack16<float> {
 // caches) and streams the gradient out.
 template <typename T>
 __global__ __launch_bounds__(kLpThreads) void logprob_bwd_kernel(LogprobBwdLaunch a) {
-  const int64_t r = blockIdx.x;
   const int tid = threadIdx.x;
   const int vocab = a.vocab;
-  T* out = reinterpret_cast<T*>(a.dlogits) + r * (int64_t)vocab;
+  // dense: workgroup = flat logit row r, output row r; gathered: workgroup =
+  // gather record, output row = record index
+  const int64_t o_row = blockIdx.x;
+  const int item = a.gathered ? (int)blockIdx.x : a.row_item[blockIdx.x];
+  const int64_t r = a.gathered ? a.rows[item].logit_row : (int64_t)blockIdx.x;
+  if (a.gathered && a.row_index && tid == 0) a.row_index[item] = (int32_t)r;
+  T* out = reinterpret_cast<T*>(a.dlogits) + o_row * (int64_t)vocab;
   constexpr int N = Vec16<T>::N;
-  const bool aligned = ((r * (int64_t)vocab * (int64_t)sizeof(T)) & 15) == 0 &&
+  const bool aligned = ((o_row * (int64_t)vocab * (int64_t)sizeof(T)) & 15) == 0 &&
+                       ((r * (int64_t)vocab * (int64_t)sizeof(T)) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.dlogits) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0;
   const int nvec = aligned ? vocab / N : 0;
-  const int item = a.row_item[r];
   if (item < 0) {
     u32x4* ov = reinterpret_cast<u32x4*>(out);
     for (int vi = tid; vi < nvec; vi += kLpThreads) __builtin_nontemporal_store(u32x4{0, 0, 0, 0}, ov + vi);
@@ -334,12 +339,16 @@ template <typename T>
 __global__ __launch_bounds__(kLpbThreads) void logprob_bwd_reg_kernel(LogprobBwdLaunch a) {
   constexpr int N = Vec16<T>::N;
   constexpr int NW = kLpbThreads / 64;
-  const int64_t r = blockIdx.x;
   const int tid = threadIdx.x;
   const int vocab = a.vocab;
   const int nvec = vocab / N;  // vocab % N == 0 here
-  u32x4* ov = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.dlogits) + r * (int64_t)vocab);
-  const int item = a.row_item[r];
+  // dense: workgroup = flat logit row r, output row r; gathered: workgroup =
+  // gather record, output row = record index
+  const int64_t o_row = blockIdx.x;
+  const int item = a.gathered ? (int)blockIdx.x : a.row_item[blockIdx.x];
+  const int64_t r = a.gathered ? a.rows[item].logit_row : (int64_t)blockIdx.x;
+  if (a.gathered && a.row_index && tid == 0) a.row_index[item] = (int32_t)r;
+  u32x4* ov = reinterpret_cast<u32x4*>(reinterpret_cast<T*>(a.dlogits) + o_row * (int64_t)vocab);
   if (item < 0) {
 #pragma unroll
     for (int j = 0; j < kLpbVecs; ++j) {
@@ -548,8 +557,9 @@ hipError_t launch_logprob(const LogprobLaunch& a, hipStream_t s) {
 }
 
 hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s) {
-  if (a.sumT <= 0) return hipSuccess;
-  TimingScope t("pp_logprob_bwd", s);
+  const int grid = a.gathered ? a.n_rows : a.sumT;
+  if (grid <= 0) return hipSuccess;
+  TimingScope t(a.gathered ? "pp_logprob_bwd_rows" : "pp_logprob_bwd", s);
   const int esz = a.dtype == kBF16 ? 2 : 4;
   const int per_vec = 16 / esz;
   // the one-read kernel needs every row to start on a 16-byte boundary and to
@@ -559,15 +569,15 @@ hipError_t launch_logprob_bwd(const LogprobBwdLaunch& a, hipStream_t s) {
                     (reinterpret_cast<uintptr_t>(a.dlogits) & 15) == 0;
   if (fits) {
     if (a.dtype == kBF16)
-      hipLaunchKernelGGL(logprob_bwd_reg_kernel<__bf16>, dim3(a.sumT), dim3(kLpbThreads), 0, s, a);
+      hipLaunchKernelGGL(logprob_bwd_reg_kernel<__bf16>, dim3(grid), dim3(kLpbThreads), 0, s, a);
     else
-      hipLaunchKernelGGL(logprob_bwd_reg_kernel<float>, dim3(a.sumT), dim3(kLpbThreads), 0, s, a);
+      hipLaunchKernelGGL(logprob_bwd_reg_kernel<float>, dim3(grid), dim3(kLpbThreads), 0, s, a);
     return hipGetLastError();
   }
   if (a.dtype == kBF16)
-    hipLaunchKernelGGL(logprob_bwd_kernel<__bf16>, dim3(a.sumT), dim3(kLpThreads), 0, s, a);
+    hipLaunchKernelGGL(logprob_bwd_kernel<__bf16>, dim3(grid), dim3(kLpThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(logprob_bwd_kernel<float>, dim3(a.sumT), dim3(kLpThreads), 0, s, a);
+    hipLaunchKernelGGL(logprob_bwd_kernel<float>, dim3(grid), dim3(kLpThreads), 0, s, a);
   return hipGetLastError();
 }
 

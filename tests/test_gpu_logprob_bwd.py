@@ -1,5 +1,9 @@
-"""GPU parity of the log-prob backward (pp_seq_logprob_bwd) against the fp64
-oracle's seq_logprob_grad, element by element.
+"""GPU parity of the log-prob backward (pp_seq_logprob_bwd, and
+pp_seq_logprob_bwd_rows, which writes only the rows that predict a response
+token) against the fp64 oracle's seq_logprob_grad, element by element.  The
+gathered rows must come back in the order of the oracle's
+logprob_predicting_rows, with those row indices (bit-exact), and equal the
+dense output's rows bit for bit.
 
 Tolerances, derived from the arithmetic: the kernel forms softmax in fp32 from
 a logsumexp accumulated in fp32 (relative error a few 1e-6 for vocabularies up
@@ -55,6 +59,19 @@ def _check_bwd(pack, V, dtype, sigma, seed, dseq=None):
     assert np.isfinite(got).all()
     err = np.abs(got - ref) - RTOL[dtype] * np.abs(ref)
     assert err.max() <= 1e-6 * gmax, err.max()
+    # the gathered form: the same rows, compact, with their indices
+    rows_want = orc.logprob_predicting_rows(*pack.oracle_args())
+    assert pp.pp_logprob_row_count(pack) == len(rows_want)
+    if rows_want:
+        dr = torch.full((len(rows_want), V), float("nan"), dtype=dtype, device=DEV)
+        ri = torch.full((len(rows_want),), -7, dtype=torch.int32, device=DEV)
+        pp.pp_seq_logprob_bwd_rows(pack, logits.to(DEV), tokens.to(DEV), dseq.to(DEV), dlogits_rows=dr,
+                                   row_index=ri)
+        assert ri.cpu().tolist() == rows_want
+        assert torch.equal(dr, dl[torch.tensor(rows_want, device=DEV).long()])
+        g_rows = dr.double().cpu().numpy()
+        err = np.abs(g_rows - ref[rows_want]) - RTOL[dtype] * np.abs(ref[rows_want])
+        assert err.max() <= 1e-6 * gmax, err.max()
     return got
 
 
@@ -133,6 +150,11 @@ def test_logprob_bwd_out_of_range_label_poisons_its_row():
     dl = pp.pp_seq_logprob_bwd(pack, logits, tokens.to(DEV), dseq).cpu()
     assert torch.isnan(dl[4]).all()
     assert torch.isfinite(dl[torch.arange(10) != 4]).all()
+    # gathered: rows 3 (first tokens), 4, 5, 7, 8 -- only row 4's copy is NaN
+    dr, ri = pp.pp_seq_logprob_bwd_rows(pack, logits, tokens.to(DEV), dseq)
+    assert ri.cpu().tolist() == [3, 4, 5, 7, 8]
+    dr = dr.cpu()
+    assert torch.isnan(dr[1]).all() and torch.isfinite(dr[[0, 2, 3, 4]]).all()
 
 
 def test_logprob_bwd_fullsize_rm_k4_sampled():
@@ -147,6 +169,12 @@ def test_logprob_bwd_fullsize_rm_k4_sampled():
     tokens = wl.randint((T,), V, seed + wl.STREAM_TOKENS, DEV)
     dseq = wl.randn((pack.num_rows, pack.max_resp), seed + 5, torch.float32, DEV)
     dl = pp.pp_seq_logprob_bwd(pack, logits, tokens, dseq)
+    # the gathered form at full size: the oracle's rows, each equal to the dense row
+    dr, ri = pp.pp_seq_logprob_bwd_rows(pack, logits, tokens, dseq)
+    rows_want = orc.logprob_predicting_rows(*pack.oracle_args())
+    assert ri.cpu().tolist() == rows_want
+    assert torch.equal(dr, dl[ri.long()])
+    del dr
     torch.cuda.synchronize()
     tok = tokens.cpu().numpy()
     g = dseq.double().cpu().numpy()

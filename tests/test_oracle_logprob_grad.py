@@ -89,3 +89,21 @@ def test_out_of_range_label_poisons_only_its_row():
     assert np.all(np.isnan(grad[t_bad - 1]))
     others = [r for r in range(pack.total_tokens) if r != t_bad - 1]
     assert np.all(np.isfinite(grad[others]))
+
+
+def test_predicting_rows_by_hand_and_by_the_gradient():
+    """The rows the gathered backward writes: a row written out by hand, the
+    pinned row count, and -- for random logits and nonzero dseq -- exactly the
+    rows where the (finite-difference pinned) gradient is not zero."""
+    # P = 3, responses of 2 and 2 tokens at 3..4 and 5..6, one padding token:
+    # row 2 predicts tokens 3 and 5, row 3 predicts 4, row 5 predicts 6
+    pack = wl.make_pack([3], [[2, 2]], pad=[1])
+    assert orc.logprob_predicting_rows(*pack.oracle_args()) == [2, 3, 5]
+    for seed, P, L, pad in ((3, [4, 1, 6], [[2, 0, 3], [1, 1], [5]], [0, 2, 1]),
+                            (4, [2, 9], [[1], [4, 4, 1, 2]], [3, 0])):
+        pack, logits, tokens, dseq = _case(seed, P, L, V=6, pad=pad)
+        args = pack.oracle_args()
+        rows = orc.logprob_predicting_rows(*args)
+        assert len(rows) == orc.logprob_rows_needed(pack.prompt_len, pack.num_resp, pack.resp_len.tolist())
+        grad = orc.seq_logprob_grad(*args, logits, tokens, np.where(dseq == 0, 1.0, dseq))
+        assert rows == sorted(np.flatnonzero(np.abs(grad).sum(axis=1) > 0).tolist())
