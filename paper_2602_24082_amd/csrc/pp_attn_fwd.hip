@@ -12,7 +12,8 @@
 //     softmax row statistics stay in the lane (one cross-half exchange);
 //   * each list entry carries, per wave, whether the wave's 32 x BN block of
 //     pairs is invisible (skipped), fully visible, or mixed; only mixed blocks
-//     evaluate the mask visible(i, j) = j <= hi_i && j is not in [P, lo_i);
+//     evaluate the mask visible(i, j) = j <= hi_i && j is not in [P, lo_i)
+//     (on blocks of the causal class the hole is known to be empty);
 //   * base-2 online softmax with scale*log2(e) folded in; the running maximum
 //     is only raised when a tile exceeds it by more than 2^8, so most tiles
 //     skip the rescale of O;
@@ -188,23 +189,20 @@ __global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(Fwd
         __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
       }
     }
-    if (cls == kWaveCausal) {
-      // only the causal edge cuts this block: key k0 + 4hf + off is visible
-      // iff off <= hi - k0 - 4hf
+    // masked pairs get S = -inf.  One branch for every block that is not fully
+    // visible (on a causal block the hole is empty, so the same test reduces to
+    // the causal edge): with a separate causal branch the compiler kept S in
+    // different registers on each path and copied all of S on full blocks.
+    if (cls != kWaveFull) {
       const int lim = hi - k0 - 4 * hf;
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[kb][r] = (kb * 32 + 8 * (r >> 2) + (r & 3)) <= lim ? s[kb][r] : kNegInf;
-    } else if (cls == kWaveMasked) {
-      const int lim = hi - k0 - 4 * hf;
+      const unsigned hole_t = cls == kWaveMasked ? hole : 0u;
       const int jp = k0 + 4 * hf - it.P;
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
-          const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole);
+          const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole_t);
           s[kb][r] = vis ? s[kb][r] : kNegInf;
         }
     }
