@@ -1,8 +1,12 @@
 // Backward attention over preference-packed rows (Sec. 3.2) on gfx950.
 //
-// Three deterministic passes (no atomics):
+// Two deterministic passes (no atomics), the query-major one first:
 //
-//   bwd_prep   delta_i = dO_i . O_i and -lse_i log2(e)  (fp32, [hq, sumT])
+//   bwd_dq     query-major, like the forward (lane = query).  Its prologue forms
+//              delta_i = dO_i . O_i and -lse_i log2(e) for its own queries (fp32,
+//              [hq, sumT]) and stores them for the dK/dV pass; then
+//                S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - delta)
+//                dQ^T += K^T dS^T
 //   bwd_dkdv   key-major: one workgroup = one 128-key tile of one kv-head and
 //              eight waves; waves w and w+4 own keys 32*(w%4) .. +31 and take the
 //              two 32-query halves of each 64-query step (two waves per SIMD).
@@ -14,12 +18,9 @@
 //              response's queries, so the shared prompt's dK/dV gather all K
 //              responses' contributions in one place.  Per step (S = Q K^T,
 //              lane = key):
-//                P  = exp2(S*scale*log2e - lse_i*log2e) (masked; -lse*log2e from bwd_prep)
+//                P  = exp2(S*scale*log2e - lse_i*log2e) (masked; -lse*log2e from bwd_dq)
 //                dP = dO V^T,  dS = P (dP - delta_i)
 //                dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T by transposed LDS reads)
-//   bwd_dq     query-major, like the forward (lane = query):
-//                S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - delta)
-//                dQ^T += K^T dS^T
 //
 // All products run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Q, K, V
 // and dO are bf16 here (fp32 callers are converted by a pre-pass); O and the
@@ -38,21 +39,19 @@
 namespace pp {
 namespace {
 
-typedef uint32_t Chunk16 __attribute__((ext_vector_type(4)));
-
 template <typename TO>
 struct BwdParams {
   const __bf16* q;
   const __bf16* k;
   const __bf16* v;
   const __bf16* dout;
-  const TO* o;       // caller dtype
-  const TO* dout_o;  // dO in the caller dtype (for delta)
+  const TO* o;       // caller dtype (for delta)
+  const TO* dout_o;  // dO in the caller dtype (for delta; fp32 callers only)
   const float* lse;
   TO* dq;
   TO* dk;
   TO* dv;
-  float* delta;
+  float* delta;  // written by the dQ pass, read by dK/dV
   float* nlse2;  // -LSE * log2(e), written next to delta
   const QTileItem* dq_items;
   const KTileEntry* dq_ktiles;
@@ -64,13 +63,6 @@ struct BwdParams {
   float scale_log2;
   const int32_t* pos;      // ROPE: position of every flat token
   const double* inv_freq;  // ROPE: [D/2]
-  // plan metadata copied by the pre-pass's workgroups from prep_blocks on:
-  // 16-byte vectors [0, stage_n16), then stage_tail (< 16) single bytes
-  const Chunk16* stage_src;
-  Chunk16* stage_dst;
-  int64_t stage_n16;
-  int stage_tail;
-  int64_t prep_blocks;
 };
 
 // Inverse rotary rotation of one lane's gradient row held in 32x32 accumulator
@@ -88,64 +80,6 @@ __device__ __forceinline__ void rope_grad_rows(Row (&v)[D / 32], const double* i
       v[m][r] = g1 * cs + g2 * sn;
       v[m + HM][r] = g2 * cs - g1 * sn;
     }
-}
-
-// ---------------------------------------------------------------------------
-// delta = rowsum(dO * O), and -LSE log2(e) in the layout the dK/dV kernel
-// stages (the exponent of P is then one fma away from S)
-// ---------------------------------------------------------------------------
-
-constexpr int kPrepRowsPerThread = 4;
-
-template <int D, typename TO>
-__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t n_rows) {
-  if (blockIdx.x >= p.prep_blocks) {
-    // the plan metadata copy (the dK/dV and dQ passes, launched after this
-    // kernel, read it; this pass does not)
-    const int64_t i = (blockIdx.x - p.prep_blocks) * 256 + threadIdx.x;
-    if (i < p.stage_n16) p.stage_dst[i] = p.stage_src[i];
-    if (i < p.stage_tail)
-      reinterpret_cast<uint8_t*>(p.stage_dst + p.stage_n16)[i] =
-          reinterpret_cast<const uint8_t*>(p.stage_src + p.stage_n16)[i];
-    return;
-  }
-  constexpr int LPR = D / 8;      // lanes per (token, head) row
-  constexpr int RPB = 256 / LPR;  // rows per block and pass
-  constexpr int RPT = kPrepRowsPerThread;
-  typedef TO vec8 __attribute__((ext_vector_type(8)));
-  const int tid = threadIdx.x;
-  const int part = tid % LPR;
-  // rows run head-major (row = h * sumT + t), the layout of lse, delta and
-  // nlse2, so a block's per-row values are contiguous; each O / dO row is a
-  // whole D-element run.  A thread's RPT rows are loaded before any is summed.
-  const int64_t row0 = (int64_t)blockIdx.x * RPB * RPT + tid / LPR;
-  vec8 a[RPT], b[RPT];
-#pragma unroll
-  for (int k = 0; k < RPT; ++k) {
-    const int64_t row = row0 + k * RPB;
-    if (row < n_rows) {
-      const int64_t h = row / p.sumT, t = row - h * p.sumT;
-      const int64_t src = (t * p.hq + h) * D + part * 8;
-      // each O and dO element is read once here: nontemporal loads (the dK/dV
-      // and dQ passes read dO as fast afterwards)
-      a[k] = __builtin_nontemporal_load(reinterpret_cast<const vec8*>(p.dout_o + src));
-      b[k] = __builtin_nontemporal_load(reinterpret_cast<const vec8*>(p.o + src));
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < RPT; ++k) {
-    const int64_t row = row0 + k * RPB;
-    float acc = 0.f;
-    if (row < n_rows) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc += (float)a[k][e] * (float)b[k][e];
-    }
-    for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-    if (row < n_rows && part == 0) {
-      p.delta[row] = acc;
-      p.nlse2[row] = -p.lse[row] * kLog2e;
-    }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -409,13 +343,39 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
   const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
   const unsigned hole = (real && lo > it.P) ? (unsigned)(lo - it.P) : 0u;
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
-  const float nlse2 = real ? -p.lse[(int64_t)head * p.sumT + it.tok0 + i] * kLog2e : 0.f;
-  const float dlt = real ? p.delta[(int64_t)head * p.sumT + it.tok0 + i] : 0.f;
   bf16x8 qf[D / 16], df[D / 16];
 #pragma unroll
   for (int c = 0; c < D / 16; ++c) {
     qf[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.q + qrow * D + 16 * c + 8 * hf) : bf16x8{};
     df[c] = in_tile ? *reinterpret_cast<const bf16x8*>(p.dout + qrow * D + 16 * c + 8 * hf) : bf16x8{};
+  }
+  // delta = dO . O of this lane's query (its half of the row, then the other
+  // half from lane l ^ 32) and -LSE log2(e); written for the dK/dV pass, which
+  // runs after this one
+  float nlse2 = 0.f, dlt = 0.f;
+  {
+    float acc = 0.f;
+    if (real) {
+      typedef TO vec8 __attribute__((ext_vector_type(8)));
+#pragma unroll
+      for (int c = 0; c < D / 16; ++c) {
+        const vec8 b = *reinterpret_cast<const vec8*>(p.o + qrow * D + 16 * c + 8 * hf);
+        if constexpr (sizeof(TO) == 2) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc += (float)df[c][e] * (float)b[e];
+        } else {
+          const vec8 a = *reinterpret_cast<const vec8*>(p.dout_o + qrow * D + 16 * c + 8 * hf);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc += (float)a[e] * (float)b[e];
+        }
+      }
+      nlse2 = -p.lse[(int64_t)head * p.sumT + it.tok0 + i] * kLog2e;
+    }
+    dlt = half_swap_sum(acc);
+    if (real && hf == 0) {
+      p.delta[(int64_t)head * p.sumT + it.tok0 + i] = dlt;
+      p.nlse2[(int64_t)head * p.sumT + it.tok0 + i] = nlse2;
+    }
   }
 
   const int64_t kv_stride = (int64_t)p.hkv * D;
@@ -562,30 +522,9 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   p.scale_log2 = a.scale * kLog2e;
   p.pos = a.pos;
   p.inv_freq = a.inv_freq;
-  const int64_t n_rows = (int64_t)a.sumT * a.hq;
-  if (n_rows == 0) return hipSuccess;
-  {
-    constexpr int RPB = 256 / (D / 8) * kPrepRowsPerThread;
-    p.prep_blocks = (n_rows + RPB - 1) / RPB;
-    p.stage_src = static_cast<const Chunk16*>(a.stage_src);
-    p.stage_dst = static_cast<Chunk16*>(a.stage_dst);
-    p.stage_n16 = (int64_t)(a.stage_bytes / 16);
-    p.stage_tail = (int)(a.stage_bytes % 16);
-    const int64_t copy_threads = p.stage_n16 > p.stage_tail ? p.stage_n16 : p.stage_tail;
-    const int64_t copy_blocks = a.stage_bytes ? (copy_threads + 255) / 256 : 0;
-    TimingScope t("pp_attn_bwd_prep", s);
-    hipLaunchKernelGGL((bwd_prep_kernel<D, TO>), dim3((unsigned)(p.prep_blocks + copy_blocks)), dim3(256), 0, s,
-                       p, n_rows);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  {
-    TimingScope t("pp_attn_bwd_dkdv", s);
-    const dim3 grid((unsigned)((int64_t)a.n_kv_items * a.hkv));
-    if (a.rope) hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, true>), grid, dim3(512), 0, s, p);
-    else hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, false>), grid, dim3(512), 0, s, p);
-  }
-  e = hipGetLastError();
+  if ((int64_t)a.sumT * a.hq == 0) return hipSuccess;
+  // the plan metadata (self-contained calls) lands before the dQ pass reads it
+  hipError_t e = a.stage_bytes ? launch_stage_copy(a.stage_src, a.stage_dst, a.stage_bytes, s) : hipSuccess;
   if (e != hipSuccess) return e;
   {
     TimingScope t("pp_attn_bwd_dq", s);
@@ -593,7 +532,16 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
     if (a.rope) hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqStages, TO, true>), grid, dim3(kDqWaves * 64), 0, s, p);
     else hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqStages, TO, false>), grid, dim3(kDqWaves * 64), 0, s, p);
   }
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  {
+    TimingScope t("pp_attn_bwd_dkdv", s);
+    const dim3 grid((unsigned)((int64_t)a.n_kv_items * a.hkv));
+    if (a.rope) hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, true>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, false>), grid, dim3(512), 0, s, p);
+  }
   return hipGetLastError();
+
 }
 
 }  // namespace

@@ -1059,8 +1059,8 @@ void bwd_image(const Batch& bt, const BwdPlan& p, int head_dim, const double* ro
 }
 
 // Enqueues the backward on metadata already staged in ws.
-// stage_src / stage_bytes: metadata still to be copied into ws (by the delta
-// pre-pass, which reads none of it), or null.
+// stage_src / stage_bytes: metadata still to be copied into ws (a copy kernel
+// ahead of the backward's passes), or null.
 pp_status bwd_launch(const BwdPlan& p, void* ws, int sumT, pp_dtype dtype, int hq, int hkv, int head_dim,
                      float scale, const void* q, const void* k, const void* v, const void* o,
                      const float* lse, const void* dout, void* dq, void* dk, void* dv, bool rope,
@@ -1145,7 +1145,7 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   const double base = rope_base ? *rope_base : 0.0;
   bwd_image(bt, p, head_dim, rope_base ? &base : nullptr, &img);
   hipStream_t s = (hipStream_t)hip_stream;
-  // the metadata copy rides in the delta pre-pass's launch
+  // the metadata copy is enqueued by the backward's launcher, ahead of its passes
   return stage_with(ws, img.buf.data(), img.buf.size(), s, [&](const void* dev_src) {
     return bwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, dout, dq, dk, dv,
                       rope_base != nullptr, s, dev_src, img.buf.size());

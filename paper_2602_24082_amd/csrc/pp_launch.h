@@ -73,8 +73,8 @@ struct AttnBwdLaunch {
   void* dq;
   void* dk;
   void* dv;
-  float* delta;              // [hq, sumT] scratch
-  float* nlse2;              // [hq, sumT] scratch: -LSE * log2(e)
+  float* delta;              // [hq, sumT] scratch, written by the dQ pass
+  float* nlse2;              // [hq, sumT] scratch: -LSE * log2(e), likewise
   const QTileItem* dq_items;
   const KTileEntry* dq_ktiles;
   int n_dq_items;
@@ -91,7 +91,7 @@ struct AttnBwdLaunch {
   const int32_t* pos = nullptr;
   const double* inv_freq = nullptr;
   // plan metadata to copy into stage_dst (16-byte aligned) from mapped pinned
-  // host memory, done by extra workgroups of the delta pre-pass; none if 0 bytes
+  // host memory by a copy kernel ahead of the dQ pass; none if 0 bytes
   const void* stage_src = nullptr;
   void* stage_dst = nullptr;
   size_t stage_bytes = 0;

@@ -128,7 +128,7 @@ def test_timing_select_times_only_the_named_launches():
         pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
         torch.cuda.synchronize()
         pp.pp_timing_enable(False)
-        assert {"pp_attn_fwd", "pp_attn_bwd_prep", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq"} <= set(pp.pp_timing_get())
+        assert {"pp_attn_fwd", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq", "pp_stage"} <= set(pp.pp_timing_get())
     finally:
         pp.pp_timing_enable(False)
         pp.pp_timing_select(None)
