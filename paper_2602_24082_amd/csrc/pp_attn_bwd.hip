@@ -242,12 +242,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     // are all visible skips the test
     const int u_first = qb0 - j;  // query - key of the half's first query
     if (wave_any(!(u_first >= 0 && (unsigned)(u_first + 31) < span))) {
+      // query u_first + 4hf + o (o = 8 r4 + e) is visible iff 0 <= that < span
+      const int base = u_first + 4 * hf;
+      const uint32_t vis = bits_below32((int)span - base) & ~bits_below32(-base);
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const unsigned u0 = (unsigned)(u_first + 8 * r4 + 4 * hf);
+      for (int r4 = 0; r4 < 4; ++r4)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) s[4 * r4 + e] = u0 + e < span ? s[4 * r4 + e] : kNegInf;
-      }
+        for (int e = 0; e < 4; ++e) s[4 * r4 + e] = keep_or_neginf(s[4 * r4 + e], vis, 8 * r4 + e);
     }
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
@@ -448,16 +449,19 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
     // its masked pairs to -inf (one test covers the causal and the general
     // class: on a causal block the hole is empty).
     if (cls != kWaveFull) {
+      // key k0 + 4hf + off is visible iff off <= hi - k0 - 4hf (causal) and it
+      // is not in the hole [P, lo), i.e. off not in [P - k0 - 4hf, + hole)
       const int lim = hi - k0 - 4 * hf;
-      const unsigned hole_t = cls == kWaveMasked ? hole : 0u;
-      const int jp = k0 + 4 * hf - it.P;
+      const int h0 = it.P - k0 - 4 * hf;
+      const int hn = cls == kWaveMasked ? (int)hole : 0;
+      const uint64_t vis = bits_below64(lim + 1) & ~(bits_below64(h0 + hn) & ~bits_below64(h0));
+      const uint32_t vis_lo = (uint32_t)vis, vis_hi = (uint32_t)(vis >> 32);
 #pragma unroll
       for (int kb = 0; kb < QKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
-          const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole_t);
-          s[kb][r] = vis ? s[kb][r] : kNegInf;
+          s[kb][r] = keep_or_neginf(s[kb][r], off < 32 ? vis_lo : vis_hi, off & 31);
         }
     }
 #pragma unroll

@@ -194,16 +194,19 @@ __global__ __launch_bounds__(NW * 64, PP_FWD_MIN_WAVES) void attn_fwd_kernel(Fwd
     // the causal edge): with a separate causal branch the compiler kept S in
     // different registers on each path and copied all of S on full blocks.
     if (cls != kWaveFull) {
+      // key k0 + 4hf + off is visible iff off <= hi - k0 - 4hf (causal) and it
+      // is not in the hole [P, lo), i.e. off not in [P - k0 - 4hf, + hole)
       const int lim = hi - k0 - 4 * hf;
-      const unsigned hole_t = cls == kWaveMasked ? hole : 0u;
-      const int jp = k0 + 4 * hf - it.P;
+      const int h0 = it.P - k0 - 4 * hf;
+      const int hn = cls == kWaveMasked ? (int)hole : 0;
+      const uint64_t vis = bits_below64(lim + 1) & ~(bits_below64(h0 + hn) & ~bits_below64(h0));
+      const uint32_t vis_lo = (uint32_t)vis, vis_hi = (uint32_t)(vis >> 32);
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int off = kb * 32 + 8 * (r >> 2) + (r & 3);
-          const bool vis = (off <= lim) & ((unsigned)(jp + off) >= hole_t);
-          s[kb][r] = vis ? s[kb][r] : kNegInf;
+          s[kb][r] = keep_or_neginf(s[kb][r], off < 32 ? vis_lo : vis_hi, off & 31);
         }
     }
     // ---- online softmax with a lazily raised reference maximum

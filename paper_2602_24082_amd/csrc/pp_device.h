@@ -261,6 +261,22 @@ constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
 constexpr int kSchedTrans = 0x400;
 
+// Visibility bitmasks of a lane's row of a block: bit o is set when the
+// block's o-th element in that row is visible.  A lane forms its mask once per
+// block from a few ranges; each element is then kept or set to -inf by one
+// signed bit extract and one bit insert, instead of compares and selects.
+__device__ __forceinline__ uint64_t bits_below64(int n) {  // bits [0, n), n of any sign
+  return n <= 0 ? 0ull : n >= 64 ? ~0ull : ((1ull << n) - 1ull);
+}
+__device__ __forceinline__ uint32_t bits_below32(int n) {
+  return n <= 0 ? 0u : n >= 32 ? ~0u : ((1u << n) - 1u);
+}
+// x where bit `bit` of `word` is set, else -inf
+__device__ __forceinline__ float keep_or_neginf(float x, uint32_t word, int bit) {
+  const int m = __builtin_amdgcn_sbfe((int)word, bit, 1);  // 0 or -1
+  return __int_as_float((__float_as_int(x) & m) | (~m & (int)0xff800000u));
+}
+
 // Wave-wide any of a lane predicate, as a value the compiler knows is uniform
 // (so a branch on it does not make a loop divergent).
 __device__ __forceinline__ bool wave_any(bool x) { return __builtin_amdgcn_readfirstlane(__any(x)) != 0; }
