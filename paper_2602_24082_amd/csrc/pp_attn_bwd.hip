@@ -1,12 +1,7 @@
 // Backward attention over preference-packed rows (Sec. 3.2) on gfx950.
 //
-// Two deterministic passes (no atomics), the query-major one first:
+// Two deterministic passes (no atomics) in one of two modes:
 //
-//   bwd_dq     query-major, like the forward (lane = query).  Its prologue forms
-//              delta_i = dO_i . O_i and -lse_i log2(e) for its own queries (fp32,
-//              [hq, sumT]) and stores them for the dK/dV pass; then
-//                S^T = K Q^T, dP^T = V dO^T, dS^T = P^T (dP^T - delta)
-//                dQ^T += K^T dS^T
 //   bwd_dkdv   key-major: one workgroup = one 128-key tile of one kv-head and
 //              eight waves; waves w and w+4 own keys 32*(w%4) .. +31 and take the
 //              two 32-query halves of each 64-query step (two waves per SIMD).
@@ -18,9 +13,22 @@
 //              response's queries, so the shared prompt's dK/dV gather all K
 //              responses' contributions in one place.  Per step (S = Q K^T,
 //              lane = key):
-//                P  = exp2(S*scale*log2e - lse_i*log2e) (masked; -lse*log2e from bwd_dq)
+//                P  = exp2(S*scale*log2e - lse_i*log2e) (masked)
 //                dP = dO V^T,  dS = P (dP - delta_i)
 //                dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T by transposed LDS reads)
+//
+//   stored dS (the default; the workspace holds one bf16 dS value per pair of
+//              every 32 x 32 block with a visible pair, per head):
+//                bwd_prep   delta_i = dO_i . O_i and -lse_i log2(e)
+//                bwd_dkdv   as above, and each wave stores its 32 x 32 dS block
+//                bwd_dq_ds  query-major: dQ^T += K^T dS^T from the stored blocks,
+//                           no recomputation of S, P or dP
+//   recompute (a workspace without the dS region: scratch linear in tokens):
+//                bwd_dq     query-major, first: its prologue forms delta and
+//                           -lse log2(e) for its queries and stores them for
+//                           dK/dV; then S^T = K Q^T, dP^T = V dO^T,
+//                           dS^T = P^T (dP^T - delta), dQ^T += K^T dS^T
+//                bwd_dkdv   as above
 //
 // All products run on v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  Q, K, V
 // and dO are bf16 here (fp32 callers are converted by a pre-pass); O and the
@@ -51,8 +59,13 @@ struct BwdParams {
   TO* dq;
   TO* dk;
   TO* dv;
-  float* delta;  // written by the dQ pass, read by dK/dV
+  float* delta;  // dO . O per (head, token): read by dK/dV
   float* nlse2;  // -LSE * log2(e), written next to delta
+  // stored-dS mode: the dS tiles and the per-key-block panels that place them
+  __bf16* ds;
+  const int32_t* row_kb0;
+  const DsPanel* kb_panel;
+  int64_t ds_tiles;  // tiles per head
   const QTileItem* dq_items;
   const KTileEntry* dq_ktiles;
   const KTileItem* kv_items;
@@ -80,6 +93,53 @@ __device__ __forceinline__ void rope_grad_rows(Row (&v)[D / 32], const double* i
       v[m][r] = g1 * cs + g2 * sn;
       v[m + HM][r] = g2 * cs - g1 * sn;
     }
+}
+
+// ---------------------------------------------------------------------------
+// delta = rowsum(dO * O) and -LSE log2(e) ahead of the stored-dS mode's dK/dV
+// pass, in the layout it stages (the exponent of P is then one fma from S)
+// ---------------------------------------------------------------------------
+
+constexpr int kPrepRowsPerThread = 4;
+
+template <int D, typename TO>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams<TO> p, int64_t n_rows) {
+  constexpr int LPR = D / 8;      // lanes per (token, head) row
+  constexpr int RPB = 256 / LPR;  // rows per block and pass
+  constexpr int RPT = kPrepRowsPerThread;
+  typedef TO vec8 __attribute__((ext_vector_type(8)));
+  const int tid = threadIdx.x;
+  const int part = tid % LPR;
+  // rows run head-major (row = h * sumT + t), the layout of lse, delta and
+  // nlse2; each O / dO row is a whole D-element run.  A thread's RPT rows are
+  // loaded before any is summed.
+  const int64_t row0 = (int64_t)blockIdx.x * RPB * RPT + tid / LPR;
+  vec8 a[RPT], b[RPT];
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int64_t row = row0 + k * RPB;
+    if (row < n_rows) {
+      const int64_t h = row / p.sumT, t = row - h * p.sumT;
+      const int64_t src = (t * p.hq + h) * D + part * 8;
+      // each O element is read once here, dO once more by dK/dV: nontemporal
+      a[k] = __builtin_nontemporal_load(reinterpret_cast<const vec8*>(p.dout_o + src));
+      b[k] = __builtin_nontemporal_load(reinterpret_cast<const vec8*>(p.o + src));
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < RPT; ++k) {
+    const int64_t row = row0 + k * RPB;
+    float acc = 0.f;
+    if (row < n_rows) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc += (float)a[k][e] * (float)b[k][e];
+    }
+    for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (row < n_rows && part == 0) {
+      p.delta[row] = acc;
+      p.nlse2[row] = -p.lse[row] * kLog2e;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -115,7 +175,11 @@ struct DkdvSmem {
   };
 };
 
-template <int D, typename TO, bool ROPE>
+// STORE_DS: each wave also stores its 32-key x 32-query block of dS (bf16,
+// the values its dK product uses) as one 2 KB tile: key row ln of the tile
+// holds the lane pair's two accumulator halves side by side (64-byte rows,
+// column c = query ds_query_of_column(c) of the block).
+template <int D, typename TO, bool ROPE, bool STORE_DS>
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   using Dma = TileDma<D, KBM / 8>;
   using KvDma = TileDma<D, KBN / 8>;
@@ -145,6 +209,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
   // padding position for a prompt key, the end of its own response for a
   // response key, 0 for padding): with i = j + u that is u < span as unsigned.
   const unsigned span = k_in_tile ? (unsigned)max(0, min(qlim, p.seg_hi[it.tok0 + j]) - j) : 0u;
+  // one past the last query that sees a key of this wave: the wave skips the
+  // tile's later query blocks (a response's keys in a tile whose range runs on
+  // through the later responses)
+  int wq_end = span ? j + (int)span : 0;
+  for (int off = 32; off > 0; off >>= 1) wq_end = max(wq_end, __shfl_xor(wq_end, off, 64));
+  wq_end = __builtin_amdgcn_readfirstlane(wq_end);
 
   const int nq = it.q_end - it.q_begin;
   const int nsteps = (nq + KBM - 1) / KBM;
@@ -195,17 +265,40 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     acc_dv[m] = f32x16{};
   }
 
+  // STORE_DS: this wave's dS tile of query block QB (row-relative) and head h
+  // is h * ds_tiles + ds_off + QB (the panel starts at the diagonal block)
+  int32_t ds_off = 0;
+  if constexpr (STORE_DS) {
+    if (wave_live) ds_off = scalar_load(&p.kb_panel[scalar_load(p.row_kb0 + it.row) + (wk0 >> 5)].off) - (wk0 >> 5);
+  }
+  bool stored = false;  // this wave's last step ended with its two dS stores
+
   int qs = it.q_begin - KBM;  // first query of the current step
+  int c_hh = 0;               // its head within the kv-head's group
   for (int n = 0; n < n_iter; ++n) {
-    qs = qs + KBM == it.q_begin + nsteps * KBM ? it.q_begin : qs + KBM;
-    wait_vmem<0>();  // this wave's part of step n (and, at n = 0, of K and V) has landed
-    __syncthreads();  // ... for every wave; the stage of step n-1 is free
+    if (qs + KBM == it.q_begin + nsteps * KBM) {
+      qs = it.q_begin;
+      ++c_hh;
+    } else {
+      qs += KBM;
+    }
+    if constexpr (STORE_DS) {
+      // this wave's part of step n has landed (and, at n = 0, of K and V);
+      // the previous step's two dS stores, issued after it, may stay in
+      // flight (vector-memory operations complete in order)
+      if (stored) wait_vmem<2>();
+      else wait_vmem<0>();
+      stored = false;
+      lds_barrier();  // ... for every wave; the stage of step n-1 is free
+    } else {
+      wait_vmem<0>();  // this wave's part of step n (and, at n = 0, of K and V) has landed
+      __syncthreads();  // ... for every wave; the stage of step n-1 is free
+    }
     if (n + 1 < n_iter) issue(n + 1);
     if (!wave_live) continue;
     const DkdvStage<D>& sg = sm.st[n & 1];
     const int qb0 = qs + qb * 32;
-    if (qb0 >= qlim) continue;
-    if (min(qb0 + 31, qlim - 1) < wk0) continue;
+    if (qb0 >= wq_end || qb0 + 31 < wk0) continue;  // no visible pair in the block
 
     // S = Q K^T and dP = dO V^T over D/16 chunks; the four fragments of chunk
     // c + 1 are read while chunk c's two MFMAs run (the scheduling groups keep
@@ -265,6 +358,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(BwdParams<TO> p) {
     }
     const bf16x8 pb0 = acc_half_to_bf16(s, 0), pb1 = acc_half_to_bf16(s, 1);
     const bf16x8 db0 = acc_half_to_bf16(dp, 0), db1 = acc_half_to_bf16(dp, 1);
+    if constexpr (STORE_DS) {
+      const int64_t tile = (int64_t)(g * G + c_hh) * p.ds_tiles + ds_off + (qb0 >> 5);
+      bf16x8* dst = reinterpret_cast<bf16x8*>(p.ds + (tile << 10)) + 4 * ln + 2 * hf;
+      dst[0] = db0;
+      dst[1] = db1;
+      stored = true;
+    }
     // dV^T += dO^T P and dK^T += Q^T dS over the half's two 16-query chunks,
     // each transposed fragment read right before its MFMA
 #pragma unroll
@@ -499,6 +599,173 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
                  f32x4{gq[m][4 * r4], gq[m][4 * r4 + 1], gq[m][4 * r4 + 2], gq[m][4 * r4 + 3]});
 }
 
+// dQ from the stored dS tiles: per 64-key tile, dQ^T += K^T dS^T with both
+// operands read transposed from LDS (the K tile shared by the workgroup, each
+// wave's two dS tiles its own).  Lane l holds query ds_query_of_column(l % 32)
+// of its wave's 32: the stored column order, which costs nothing since each
+// lane writes its own query's row.  A key block without a stored tile for this
+// wave's query block has no visible pair with it and is skipped.  The dS tiles
+// stream from HBM (each is read once), so they are fetched two tiles ahead in
+// a ring of three; the K tiles (re-read by every query tile of the row, mostly
+// from L2) one tile ahead.  The tiles' metadata (first key, and which dS tile
+// each key block reads) is gathered by the lanes 64 tiles at a time and taken
+// per tile with v_readlane: scalar loads in the loop would each stall the wave
+// (a pending scalar load also turns every LDS wait into a full one).
+template <int D, int NW, typename TO, bool ROPE>
+__global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_ds_kernel(BwdParams<TO> p) {
+  constexpr int NSK = 2, NSD = 3;
+  constexpr int RPW = QBN / NW;
+  static_assert(QKB == 2, "two 32-key blocks per key tile");
+  using Dma = TileDma<D, RPW>;
+  __shared__ __attribute__((aligned(1024))) __bf16 sK[NSK][QBN * D];
+  __shared__ __attribute__((aligned(1024))) __bf16 sD[NSD][NW][QKB][32 * 32];
+
+  int item_idx, head;
+  item_and_head(blockIdx.x, p.hq, item_idx, head);
+  const QTileItem it = load_uniform(p.dq_items + item_idx);
+  const int G = p.hq / p.hkv;
+  const int g = head / G;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63;
+  const int ln = lane & 31;
+  const int hf = lane >> 5;
+
+  const int i = it.q0 + wave * 32 + ds_query_of_column(ln);
+  const bool in_tile = i < it.q_end;
+  const int QB = (it.q0 >> 5) + wave;  // this wave's query block (row-relative)
+  const int kb_row = scalar_load(p.row_kb0 + it.row);
+  const __bf16* ds_head = p.ds + (((int64_t)head * p.ds_tiles) << 10);
+
+  const int64_t kv_stride = (int64_t)p.hkv * D;
+  const __bf16* kbase = p.k + ((int64_t)it.tok0 * p.hkv + g) * D;
+  const int n_tiles = it.kt_cnt;
+  const KTileEntry* ktiles = p.dq_ktiles + it.kt_off;
+
+  // lane l's tile c*64 + l: first key and, per key block, the dS tile within
+  // the head's region, or -1 (no visible pair with this wave's queries)
+  int v_k0 = 0, v_d0 = -1, v_d1 = -1;
+  auto stored_tile = [&](int KB) -> int {
+    if (KB * 32 >= it.valid) return -1;
+    const DsPanel pn = p.kb_panel[kb_row + KB];
+    const int rel = QB - KB;
+    return (rel >= 0 && rel < pn.len) ? pn.off + rel : -1;
+  };
+  auto gather = [&](int c) {
+    const int u = c * 64 + lane;
+    v_k0 = 0;
+    v_d0 = v_d1 = -1;
+    if (u < n_tiles) {
+      v_k0 = ktiles[u].k0;
+      v_d0 = stored_tile(v_k0 >> 5);
+      v_d1 = stored_tile((v_k0 >> 5) + 1);
+    }
+  };
+  struct TileInfo {
+    int k0, d0, d1;
+  };
+  auto info = [&](int u) {
+    const int l = u & 63;
+    return TileInfo{__builtin_amdgcn_readlane(v_k0, l), __builtin_amdgcn_readlane(v_d0, l),
+                    __builtin_amdgcn_readlane(v_d1, l)};
+  };
+
+  Dma dma;
+  dma.init(wave * RPW, kv_stride, lane);
+  auto issue_k = [&](int u, int k0) { dma.issue(sK[u % NSK], kbase + k0 * kv_stride, min(QBN, it.valid - k0)); };
+  // this wave's dS tiles of key tile u; returns the DMA instructions issued
+  auto issue_d = [&](int u, const TileInfo& f) -> int {
+    int n = 0;
+    if (f.d0 >= 0) {
+      const __bf16* src = ds_head + ((int64_t)f.d0 << 10) + 8 * lane;
+      lds_dma16(src, sD[u % NSD][wave][0]);
+      lds_dma16(src + 512, sD[u % NSD][wave][0] + 512);
+      n += 2;
+    }
+    if (f.d1 >= 0) {
+      const __bf16* src = ds_head + ((int64_t)f.d1 << 10) + 8 * lane;
+      lds_dma16(src, sD[u % NSD][wave][1]);
+      lds_dma16(src + 512, sD[u % NSD][wave][1] + 512);
+      n += 2;
+    }
+    return n;
+  };
+  // issue order K(0), dS(0), dS(1), then per tile t: K(t+1), dS(t+2).  At the
+  // top of tile t only the last group, dS(t+1) (`pend` instructions), may still
+  // be in flight: vector-memory operations complete in order.
+  int pend = 0;
+  TileInfo cur{0, -1, -1}, n1{0, -1, -1};
+  if (n_tiles > 0) {
+    gather(0);
+    cur = info(0);
+    issue_k(0, cur.k0);
+    issue_d(0, cur);
+    if (n_tiles > 1) {
+      n1 = info(1);
+      pend = issue_d(1, n1);
+    }
+  }
+
+  f32x16 acc[D / 32];
+#pragma unroll
+  for (int m = 0; m < D / 32; ++m) acc[m] = f32x16{};
+
+  for (int t = 0; t < n_tiles; ++t) {
+    if (pend >= 4) wait_vmem<4>();
+    else if (pend >= 2) wait_vmem<2>();
+    else wait_vmem<0>();
+    __syncthreads();  // K(t) landed for every wave; its stage of tile t-1 is free
+    if (t + 1 < n_tiles) issue_k(t + 1, n1.k0);
+    TileInfo n2{0, -1, -1};
+    pend = 0;
+    if (t + 2 < n_tiles) {
+      if (((t + 2) & 63) == 0) gather((t + 2) >> 6);
+      n2 = info(t + 2);
+      pend = issue_d(t + 2, n2);
+    }
+    // every fragment of a block is read before its MFMAs
+    const __bf16* sk = sK[t % NSK];
+    const bool s0 = cur.d0 >= 0, s1 = cur.d1 >= 0;
+    bf16x8 fa[2][2][D / 32], fb[2][2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      if (b == 0 ? !s0 : !s1) continue;
+      const __bf16* sd = sD[t % NSD][wave][b];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        fb[b][h] = lds_tr8_tile32(sd, 16 * h, lane);
+#pragma unroll
+        for (int m = 0; m < D / 32; ++m) fa[b][h][m] = lds_tr8<D>(sk, 32 * b + 16 * h, 32 * m, lane);
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      if (b == 0 ? !s0 : !s1) continue;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int m = 0; m < D / 32; ++m) acc[m] = mfma32(fa[b][h][m], fb[b][h], acc[m]);
+    }
+    cur = n1;
+    n1 = n2;
+  }
+
+  if (!in_tile) return;
+#pragma unroll
+  for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[m][r] *= p.scale;
+  if constexpr (ROPE) rope_grad_rows<D>(acc, p.inv_freq, p.pos[it.tok0 + i], hf);
+  TO* row = p.dq + ((int64_t)(it.tok0 + i) * p.hq + head) * D;
+#pragma unroll
+  for (int m = 0; m < D / 32; ++m)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4)
+      store4<TO>(row + 32 * m + 8 * r4 + 4 * hf,
+                 f32x4{acc[m][4 * r4], acc[m][4 * r4 + 1], acc[m][4 * r4 + 2], acc[m][4 * r4 + 3]});
+}
+
 template <int D, typename TO>
 hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   BwdParams<TO> p;
@@ -526,10 +793,38 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   p.scale_log2 = a.scale * kLog2e;
   p.pos = a.pos;
   p.inv_freq = a.inv_freq;
-  if ((int64_t)a.sumT * a.hq == 0) return hipSuccess;
-  // the plan metadata (self-contained calls) lands before the dQ pass reads it
+  p.ds = a.ds;
+  p.row_kb0 = a.row_kb0;
+  p.kb_panel = a.kb_panel;
+  p.ds_tiles = a.ds_tiles;
+  const int64_t n_rows = (int64_t)a.sumT * a.hq;
+  if (n_rows == 0) return hipSuccess;
+  // the plan metadata (self-contained calls) lands before the first pass reads it
   hipError_t e = a.stage_bytes ? launch_stage_copy(a.stage_src, a.stage_dst, a.stage_bytes, s) : hipSuccess;
   if (e != hipSuccess) return e;
+  if (a.ds) {
+    {
+      constexpr int RPB = 256 / (D / 8) * kPrepRowsPerThread;
+      TimingScope t("pp_attn_bwd_prep", s);
+      hipLaunchKernelGGL((bwd_prep_kernel<D, TO>), dim3((unsigned)((n_rows + RPB - 1) / RPB)), dim3(256), 0, s, p,
+                         n_rows);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    {
+      TimingScope t("pp_attn_bwd_dkdv", s);
+      const dim3 grid((unsigned)((int64_t)a.n_kv_items * a.hkv));
+      if (a.rope) hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, true, true>), grid, dim3(512), 0, s, p);
+      else hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, false, true>), grid, dim3(512), 0, s, p);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    {
+      TimingScope t("pp_attn_bwd_dq", s);
+      const dim3 grid((unsigned)((int64_t)a.n_dq_items * a.hq));
+      if (a.rope) hipLaunchKernelGGL((bwd_dq_ds_kernel<D, kDqWaves, TO, true>), grid, dim3(kDqWaves * 64), 0, s, p);
+      else hipLaunchKernelGGL((bwd_dq_ds_kernel<D, kDqWaves, TO, false>), grid, dim3(kDqWaves * 64), 0, s, p);
+    }
+    return hipGetLastError();
+  }
   {
     TimingScope t("pp_attn_bwd_dq", s);
     const dim3 grid((unsigned)((int64_t)a.n_dq_items * a.hq));
@@ -541,8 +836,8 @@ hipError_t launch_bwd_t(const AttnBwdLaunch& a, hipStream_t s) {
   {
     TimingScope t("pp_attn_bwd_dkdv", s);
     const dim3 grid((unsigned)((int64_t)a.n_kv_items * a.hkv));
-    if (a.rope) hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, true>), grid, dim3(512), 0, s, p);
-    else hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, false>), grid, dim3(512), 0, s, p);
+    if (a.rope) hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, true, false>), grid, dim3(512), 0, s, p);
+    else hipLaunchKernelGGL((bwd_dkdv_kernel<D, TO, false, false>), grid, dim3(512), 0, s, p);
   }
   return hipGetLastError();
 

@@ -213,6 +213,40 @@ __device__ __forceinline__ bf16x8 lds_tr8(const __bf16* tile, int row16, int col
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// A 32 x 32 bf16 tile of dS as the backward stores it: 32 key rows of 64
+// bytes, no swizzle.  The key-major pass (lane = key) writes a lane pair's two
+// accumulator halves side by side, so column c of a row holds query
+// ds_query_of_column(c) of the block: bits (c4 c3 c2 c1 c0) -> (c3 c2 c4 c1 c0),
+// the order in which a 32x32 accumulator's registers hold their rows.
+__device__ __forceinline__ int ds_query_of_column(int c) {
+  return 16 * ((c >> 3) & 1) + 8 * ((c >> 2) & 1) + 4 * (c >> 4) + (c & 3);
+}
+
+// B operand of a 32x32x16 MFMA from such a tile read transposed: lane l gets
+// column l % 32 of rows row16 + perm16(kk) (the row order of lds_tr8).  Each
+// ds_read_b64_tr_b16 covers eight whole 64-byte rows: no bank conflicts.
+__device__ __forceinline__ bf16x8 lds_tr8_tile32(const __bf16* tile, int row16, int lane) {
+  const int g = lane >> 4, a = lane & 15;
+  const int r0 = row16 + 4 * (g >> 1) + (a >> 2);
+  const int col = 16 * (g & 1) + 4 * (a & 3);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(tile + r0 * 32 + col));
+  const i16x4 hi =
+      __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(tile + (r0 + 8) * 32 + col));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Workgroup barrier that orders LDS accesses only (s_waitcnt lgkmcnt(0);
+// s_barrier): global stores issued before it stay in flight, where
+// __syncthreads would wait for them.  LDS filled by DMA is published by an
+// explicit wait_vmem ahead of it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Waits until pipelined tile t has landed, given that tiles t+1 ..
 // min(t+NS-2, n-1) (each PER_TILE DMA instructions of this wave, issued after
 // tile t) may still be in flight.  Vector-memory loads complete in order.

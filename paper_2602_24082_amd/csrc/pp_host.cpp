@@ -252,6 +252,18 @@ void build_qplan(const Batch& bt, int BM, int BN, QPlan* out) {
                    [](const QTileItem& a, const QTileItem& b) { return a.kt_cnt > b.kt_cnt; });
 }
 
+// One past the last query that sees a key of [k0, k_end), k0 < r.valid: a
+// prompt key is seen by every later real token; when the keys lie in
+// responses, the last real key's response bounds the range.
+int32_t key_tile_q_end(const Row& r, int32_t k0, int32_t k_end) {
+  if (k0 < r.P) return r.valid;
+  const int32_t last = std::min(k_end, r.valid) - 1;
+  int32_t end = r.valid;
+  for (int k = 0; k < r.K; ++k)
+    if (r.off[k] <= last && last < r.off[k] + r.len[k]) end = r.off[k] + r.len[k];
+  return end;
+}
+
 void build_kplan(const Batch& bt, int BN, std::vector<KTileItem>* out) {
   out->clear();
   for (int b = 0; b < bt.B; ++b) {
@@ -268,16 +280,7 @@ void build_kplan(const Batch& bt, int BN, std::vector<KTileItem>* out) {
         it.q_begin = it.q_end = k0;  // padding keys: nothing sees them
       } else {
         it.q_begin = k0;  // query k0 sees key k0
-        if (k0 < r.P) {
-          it.q_end = r.valid;  // a prompt key is seen by every later real token
-        } else {
-          // keys lie in responses; the last real key's response bounds the range
-          const int32_t last = std::min(it.k_end, r.valid) - 1;
-          int32_t end = r.valid;
-          for (int k = 0; k < r.K; ++k)
-            if (r.off[k] <= last && last < r.off[k] + r.len[k]) end = r.off[k] + r.len[k];
-          it.q_end = end;
-        }
+        it.q_end = key_tile_q_end(r, k0, it.k_end);
       }
       out->push_back(it);
     }
@@ -307,6 +310,38 @@ void build_seg_hi(const Batch& bt, std::vector<int32_t>* out) {
   out->assign(bt.sumT, 0);
   for (const Row& r : bt.rows)
     for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_end(r, t);
+}
+
+// Panels of the stored dS: per row, per 32-key block KB, the query blocks
+// KB .. ceil(q_end / 32) - 1, where q_end is one past the last query that sees
+// one of the block's keys within its key tile of BN keys (the tile's query
+// range clipped to the row's real tokens, and each key's own seg_end) --
+// exactly the 32 x 32 blocks that the key-major pass computes for it --
+// numbered consecutively in row and block order.  Returns the tiles per head,
+// or -1 if they do not fit 32-bit tile offsets.
+int64_t build_ds_panels(const Batch& bt, int BN, std::vector<int32_t>* row_kb0, std::vector<DsPanel>* panels) {
+  row_kb0->clear();
+  panels->clear();
+  int64_t off = 0;
+  for (const Row& r : bt.rows) {
+    row_kb0->push_back((int32_t)panels->size());
+    for (int32_t kb = 0; kb * 32 < r.T; ++kb) {
+      const int32_t k0 = kb * 32 / BN * BN, k_end = std::min(r.T, k0 + BN);
+      int32_t q_end = 0;
+      if (k0 < r.valid) {
+        const int32_t qlim = std::min(key_tile_q_end(r, k0, k_end), r.valid);
+        for (int32_t j = kb * 32; j < std::min(k_end, kb * 32 + 32); ++j) {
+          const int32_t last = std::min(qlim, seg_end(r, j));  // key j is seen by queries j .. last - 1
+          if (last > j) q_end = std::max(q_end, last);
+        }
+      }
+      const int32_t len = std::max(0, (q_end + 31) / 32 - kb);
+      panels->push_back(DsPanel{(int32_t)off, len});
+      off += len;
+      if (off > INT32_MAX) return -1;
+    }
+  }
+  return off;
 }
 
 // Position ID of row-relative token t (Sec. 3.2: each token keeps the position
@@ -570,12 +605,20 @@ void plan_fwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, FwdPlan* 
   }
 }
 
+// The backward's workspace ends with the stored-dS region (hq x ds_tiles
+// tiles of 32 x 32 bf16); a workspace that stops before it (lean_total bytes)
+// selects the recompute mode.
 struct BwdPlan {
   QPlan dq;
   std::vector<KTileItem> kv;
   std::vector<int32_t> seg_lo, seg_hi;
+  std::vector<int32_t> row_kb0;
+  std::vector<DsPanel> panels;
+  int64_t ds_tiles = 0;  // per head; -1: the stored mode is not offered
   Layout lay;
-  size_t r_seg, r_seg_hi, r_dq_items, r_dq_kt, r_kv_items, r_pos, r_freq, r_delta, r_nlse2;
+  size_t r_seg, r_seg_hi, r_dq_items, r_dq_kt, r_kv_items, r_row_kb0, r_panels, r_pos, r_freq, r_delta, r_nlse2;
+  size_t r_ds = 0;
+  size_t lean_total = 0;
   CastRegions cast;
 };
 
@@ -590,6 +633,9 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
   p->r_dq_items = p->lay.add(p->dq.items.size() * sizeof(QTileItem));
   p->r_dq_kt = p->lay.add(p->dq.ktiles.size() * sizeof(KTileEntry));
   p->r_kv_items = p->lay.add(p->kv.size() * sizeof(KTileItem));
+  p->ds_tiles = build_ds_panels(bt, kBwdBlockN, &p->row_kb0, &p->panels);
+  p->r_row_kb0 = p->lay.add(p->row_kb0.size() * 4);
+  p->r_panels = p->lay.add(p->panels.size() * sizeof(DsPanel));
   p->r_pos = p->lay.add((size_t)bt.sumT * 4);
   p->r_freq = p->lay.add((size_t)d / 2 * 8);
   p->lay.meta_bytes = p->lay.total;
@@ -602,6 +648,8 @@ void plan_bwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, BwdPlan* 
     p->cast.v = p->lay.add((size_t)bt.sumT * hkv * d * 2);
     p->cast.dout = p->lay.add((size_t)bt.sumT * hq * d * 2);
   }
+  p->lean_total = p->lay.total;
+  if (p->ds_tiles >= 0) p->r_ds = p->lay.add((size_t)p->ds_tiles * hq * 2048);
 }
 
 // One workspace layout serves the log-prob forward and its backward: the
@@ -1048,6 +1096,8 @@ void bwd_image(const Batch& bt, const BwdPlan& p, int head_dim, const double* ro
   img.put(p.lay.regions[p.r_dq_items], p.dq.items.data(), p.dq.items.size() * sizeof(QTileItem));
   img.put(p.lay.regions[p.r_dq_kt], p.dq.ktiles.data(), p.dq.ktiles.size() * sizeof(KTileEntry));
   img.put(p.lay.regions[p.r_kv_items], p.kv.data(), p.kv.size() * sizeof(KTileItem));
+  img.put(p.lay.regions[p.r_row_kb0], p.row_kb0.data(), p.row_kb0.size() * 4);
+  img.put(p.lay.regions[p.r_panels], p.panels.data(), p.panels.size() * sizeof(DsPanel));
   std::vector<int32_t> pos;
   std::vector<double> freq;
   if (rope_base) {
@@ -1063,7 +1113,7 @@ void bwd_image(const Batch& bt, const BwdPlan& p, int head_dim, const double* ro
 // ahead of the backward's passes), or null.
 pp_status bwd_launch(const BwdPlan& p, void* ws, int sumT, pp_dtype dtype, int hq, int hkv, int head_dim,
                      float scale, const void* q, const void* k, const void* v, const void* o,
-                     const float* lse, const void* dout, void* dq, void* dk, void* dv, bool rope,
+                     const float* lse, const void* dout, void* dq, void* dk, void* dv, bool rope, bool store_ds,
                      hipStream_t s, const void* stage_src = nullptr, size_t stage_bytes = 0) {
   hipError_t e;
   const void* dout_bf = dout;
@@ -1113,6 +1163,12 @@ pp_status bwd_launch(const BwdPlan& p, void* ws, int sumT, pp_dtype dtype, int h
     a.pos = (const int32_t*)at(ws, p.lay, p.r_pos);
     a.inv_freq = (const double*)at(ws, p.lay, p.r_freq);
   }
+  if (store_ds) {
+    a.ds = (__bf16*)at(ws, p.lay, p.r_ds);
+    a.row_kb0 = (const int32_t*)at(ws, p.lay, p.r_row_kb0);
+    a.kb_panel = (const DsPanel*)at(ws, p.lay, p.r_panels);
+    a.ds_tiles = p.ds_tiles;
+  }
   a.stage_src = stage_src;
   a.stage_dst = ws;
   a.stage_bytes = stage_src ? stage_bytes : 0;
@@ -1135,10 +1191,12 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   if ((st = check_bwd_ptrs(bt.sumT, q, k, v, o, lse, dout, dq, dk, dv)) != PP_OK) return st;
   BwdPlan p;
   plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
-  if (ws_bytes < p.lay.total)
-    return fail(PP_ERR_WORKSPACE_TOO_SMALL, "backward needs %zu workspace bytes, got %zu", p.lay.total,
-                ws_bytes);
-  if (p.lay.total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  if (ws_bytes < p.lean_total)
+    return fail(PP_ERR_WORKSPACE_TOO_SMALL,
+                "backward needs %zu workspace bytes (%zu without the stored dS), got %zu", p.lay.total,
+                p.lean_total, ws_bytes);
+  const bool store_ds = p.ds_tiles >= 0 && ws_bytes >= p.lay.total;
+  if (p.lean_total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
   if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (bt.sumT == 0) return PP_OK;
   MetaImage img;
@@ -1148,7 +1206,7 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   // the metadata copy is enqueued by the backward's launcher, ahead of its passes
   return stage_with(ws, img.buf.data(), img.buf.size(), s, [&](const void* dev_src) {
     return bwd_launch(p, ws, bt.sumT, dtype, hq, hkv, head_dim, scale, q, k, v, o, lse, dout, dq, dk, dv,
-                      rope_base != nullptr, s, dev_src, img.buf.size());
+                      rope_base != nullptr, store_ds, s, dev_src, img.buf.size());
   });
 }
 
@@ -1188,6 +1246,7 @@ struct pp_plan {
   pp::BwdPlan bwd;
   void* ws;        // caller's workspace: forward region first, backward at bwd_off
   size_t bwd_off;
+  bool store_ds;   // the workspace holds the backward's stored-dS region
 };
 
 namespace pp {
@@ -1228,6 +1287,17 @@ pp_status pp_plan_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int h
   return PP_OK;
 }
 
+pp_status pp_bwd_recompute_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+                                          size_t* bwd, size_t* plan) {
+  Batch bt;
+  pp_plan p{};
+  pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, nullptr, &bt, &p);
+  if (st != PP_OK) return st;
+  if (bwd) *bwd = p.bwd.lean_total;
+  if (plan) *plan = p.bwd_off + p.bwd.lean_total;
+  return PP_OK;
+}
+
 pp_status pp_plan_create(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                          const float* rope_base, void* ws, size_t ws_bytes, void* hip_stream, pp_plan** plan) {
   if (!plan) return fail(PP_ERR_INVALID_ARGUMENT, "plan is NULL");
@@ -1236,10 +1306,12 @@ pp_status pp_plan_create(const pp_pack_desc* desc, pp_dtype dtype, int hq, int h
   if (!p) return fail(PP_ERR_INVALID_ARGUMENT, "out of host memory for the plan");
   Batch bt;
   pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, rope_base, &bt, p);
-  const size_t total = p->bwd_off + p->bwd.lay.total;
-  if (st == PP_OK && ws_bytes < total)
-    st = fail(PP_ERR_WORKSPACE_TOO_SMALL, "the plan needs %zu workspace bytes, got %zu", total, ws_bytes);
-  if (st == PP_OK && total && !ws) st = fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
+  const size_t total = p->bwd_off + p->bwd.lay.total, lean = p->bwd_off + p->bwd.lean_total;
+  if (st == PP_OK && ws_bytes < lean)
+    st = fail(PP_ERR_WORKSPACE_TOO_SMALL, "the plan needs %zu workspace bytes (%zu without the stored dS), got %zu",
+              total, lean, ws_bytes);
+  p->store_ds = p->bwd.ds_tiles >= 0 && ws_bytes >= total;
+  if (st == PP_OK && lean && !ws) st = fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
   if (st == PP_OK && ws && !aligned256(ws)) st = fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
   if (st == PP_OK && bt.sumT > 0) {
     // one image: the forward's metadata at 0, the backward's at bwd_off
@@ -1287,7 +1359,7 @@ pp_status pp_attn_bwd_planned(const pp_plan* plan, float scale, const void* q, c
   if (plan->sumT == 0) return PP_OK;
   void* ws_b = static_cast<char*>(plan->ws) + plan->bwd_off;
   return bwd_launch(plan->bwd, ws_b, plan->sumT, plan->dtype, plan->hq, plan->hkv, plan->head_dim, scale, q, k, v, o,
-                    lse, dout, dq, dk, dv, plan->rope, (hipStream_t)hip_stream);
+                    lse, dout, dq, dk, dv, plan->rope, plan->store_ds, (hipStream_t)hip_stream);
 }
 
 pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,

@@ -73,8 +73,8 @@ struct AttnBwdLaunch {
   void* dq;
   void* dk;
   void* dv;
-  float* delta;              // [hq, sumT] scratch, written by the dQ pass
-  float* nlse2;              // [hq, sumT] scratch: -LSE * log2(e), likewise
+  float* delta;              // [hq, sumT] scratch: dO . O per query
+  float* nlse2;              // [hq, sumT] scratch: -LSE * log2(e)
   const QTileItem* dq_items;
   const KTileEntry* dq_ktiles;
   int n_dq_items;
@@ -90,8 +90,16 @@ struct AttnBwdLaunch {
   bool rope = false;
   const int32_t* pos = nullptr;
   const double* inv_freq = nullptr;
+  // stored-dS mode (ds non-null): dK/dV stores dS as 32 x 32 bf16 tiles, at
+  // tile (head * ds_tiles + panel.off + QB - KB) for query block QB of key
+  // block KB, and the dQ pass reads them instead of recomputing S and dP.
+  // row_kb0[b] = global index of row b's first 32-key block in kb_panel.
+  __bf16* ds = nullptr;
+  const int32_t* row_kb0 = nullptr;
+  const DsPanel* kb_panel = nullptr;
+  int64_t ds_tiles = 0;
   // plan metadata to copy into stage_dst (16-byte aligned) from mapped pinned
-  // host memory by a copy kernel ahead of the dQ pass; none if 0 bytes
+  // host memory ahead of the backward's first pass; none if 0 bytes
   const void* stage_src = nullptr;
   void* stage_dst = nullptr;
   size_t stage_bytes = 0;

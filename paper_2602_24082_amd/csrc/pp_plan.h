@@ -112,6 +112,15 @@ struct KTileItem {
   int32_t row;
 };
 
+// Where the backward keeps dS of one 32-key block (row-relative block KB of
+// a row): the block's visible pairs lie in the query blocks KB .. KB + len - 1
+// (from the diagonal to the end of its key tile's query range), stored as
+// len consecutive 32 x 32 bf16 tiles from tile `off` of each head's region.
+struct DsPanel {
+  int32_t off;
+  int32_t len;
+};
+
 // Gather record of the log-prob pass: one logit row and the labels it predicts.
 struct LogitRowItem {
   int64_t logit_row;  // flat row of the logits matrix

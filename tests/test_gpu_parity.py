@@ -38,9 +38,12 @@ def _poisoned_like(t):
     return torch.full_like(t, float("nan"))
 
 
-def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None, grads=("dq", "dk", "dv")):
-    print(f"case rows={pack.num_rows} T={pack.total_tokens} hq={hq} hkv={hkv} d={d} {dtype} seed={seed}",
-          flush=True)
+def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None, grads=("dq", "dk", "dv"),
+                     recompute=False):
+    """Forward and backward against the oracle; recompute selects the backward
+    mode that recomputes S and dP in the dQ pass instead of reading stored dS."""
+    print(f"case rows={pack.num_rows} T={pack.total_tokens} hq={hq} hkv={hkv} d={d} {dtype} seed={seed}"
+          f" recompute={recompute}", flush=True)
     q, k, v, do = _inputs(pack, hq, hkv, d, dtype, seed) if inputs is None else inputs
     qg, kg, vg, dog = (x.to(DEV) for x in (q, k, v, do))
     T = pack.total_tokens
@@ -61,7 +64,7 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
     if not check_bwd:
         return
     dq, dk, dv = _poisoned_like(qg), _poisoned_like(kg), _poisoned_like(vg)
-    pp.pp_attn_bwd(pack, qg, kg, vg, o, lse, dog, dq=dq, dk=dk, dv=dv)
+    pp.pp_attn_bwd(pack, qg, kg, vg, o, lse, dog, dq=dq, dk=dk, dv=dv, recompute=recompute)
     dq_r, dk_r, dv_r = orc.attn_bwd(*args, qn, kn, vn, don)
     out = {}
     for name, got, ref in (("dq", dq, dq_r), ("dk", dk, dk_r), ("dv", dv, dv_r)):
@@ -82,18 +85,20 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
     return out
 
 
-def test_tiny_fp32_config():
+@pytest.mark.parametrize("recompute", [False, True])
+def test_tiny_fp32_config(recompute):
     """4 rows, 4 heads (MHA), d 64, fp32 inputs, K=2 (the tiny check config)."""
     cfg = wl.CONFIGS[0]
-    _check_attention(wl.config_pack(cfg), cfg.hq, cfg.hkv, cfg.head_dim, torch.float32, 11)
+    _check_attention(wl.config_pack(cfg), cfg.hq, cfg.hkv, cfg.head_dim, torch.float32, 11, recompute=recompute)
 
 
+@pytest.mark.parametrize("recompute", [False, True])
 @pytest.mark.parametrize("d", [64, 128])
-def test_bf16_gqa_ragged(d):
+def test_bf16_gqa_ragged(d, recompute):
     """Several tiles per row, unaligned boundaries, padding, GQA 8/2."""
     pack = wl.make_pack([300, 0, 129, 5, 64], [[70, 45], [33, 64], [1, 0, 200], [130], [64, 64]],
                         pad=[3, 0, 0, 17, 0])
-    _check_attention(pack, 8, 2, d, torch.bfloat16, 21 + d)
+    _check_attention(pack, 8, 2, d, torch.bfloat16, 21 + d, recompute=recompute)
 
 
 def test_bf16_k4_mha():
@@ -101,15 +106,16 @@ def test_bf16_k4_mha():
     _check_attention(pack, 4, 4, 128, torch.bfloat16, 31)
 
 
-def test_edge_cases():
+@pytest.mark.parametrize("recompute", [False, True])
+def test_edge_cases(recompute):
     """Single response (plain causal), empty prompt (document masking), one-token
     rows, empty rows, all-padding rows, rows shorter than one tile."""
     pack = wl.make_pack([0, 1, 7, 0, 129, 3, 0],
                         [[1], [], [0, 0], [], [], [1, 1, 1], [5, 6]],
                         pad=[0, 0, 0, 0, 0, 2, 0])
-    _check_attention(pack, 4, 1, 64, torch.bfloat16, 41)
+    _check_attention(pack, 4, 1, 64, torch.bfloat16, 41, recompute=recompute)
     pack = wl.make_pack([5, 0], [[], []], pad=[0, 9])  # all-padding second row
-    _check_attention(pack, 2, 2, 128, torch.bfloat16, 42)
+    _check_attention(pack, 2, 2, 128, torch.bfloat16, 42, recompute=recompute)
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -117,7 +123,8 @@ def test_random_pack_sweep(seed):
     """Seeded random packs: prompt lengths 0-400 (the first row has none on two
     seeds: its responses are then separate documents), 0-4 responses of 0-260
     tokens, 0-20 padding tokens, GQA ratios 1, 2, 4 and 8, d 64 or 128; forward
-    and all three gradients against the oracle."""
+    and all three gradients against the oracle (odd seeds: the recompute
+    backward)."""
     rng = np.random.default_rng(1000 + seed)
     B = int(rng.integers(1, 5))
     P, L, pad = [], [], []
@@ -134,7 +141,7 @@ def test_random_pack_sweep(seed):
     hkv = int(rng.choice([1, 2, 4]))
     G = int(rng.choice([1, 2, 4, 8]))
     d = int(rng.choice([64, 128]))
-    _check_attention(pack, hkv * G, hkv, d, torch.bfloat16, 2000 + seed)
+    _check_attention(pack, hkv * G, hkv, d, torch.bfloat16, 2000 + seed, recompute=bool(seed % 2))
 
 
 def test_large_scores():
@@ -211,16 +218,33 @@ def test_g8_long_prefix_small():
     _check_attention(pack, 16, 2, 128, torch.bfloat16, 51)
 
 
-def test_backward_is_deterministic():
+@pytest.mark.parametrize("recompute", [False, True])
+def test_backward_is_deterministic(recompute):
     pack = wl.make_pack([400, 150], [[100, 61], [33, 270]])
     q, k, v, do = (x.to(DEV) for x in _inputs(pack, 8, 2, 128, torch.bfloat16, 61))
     o, lse = pp.pp_attn_fwd(pack, q, k, v)
-    g1 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
-    g2 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+    g1 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, recompute=recompute)
+    g2 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, recompute=recompute)
     o2, lse2 = pp.pp_attn_fwd(pack, q, k, v)
     assert torch.equal(o, o2) and torch.equal(lse, lse2)
     for a, b in zip(g1, g2):
         assert torch.equal(a, b)
+
+
+def test_stored_and_recompute_backward_agree():
+    """The two backward modes take the same inputs to the same gradients: dV
+    (which does not use delta) bit for bit, dQ and dK up to the rounding of
+    delta's fp32 sum and of dS to bf16 (each mode forms dS in its own pass)."""
+    pack = wl.make_pack([333, 90, 0], [[129, 64, 1, 40], [300], [65, 31]], pad=[5, 0, 11])
+    q, k, v, do = (x.to(DEV) for x in _inputs(pack, 8, 2, 128, torch.bfloat16, 71))
+    o, lse = pp.pp_attn_fwd(pack, q, k, v)
+    s = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+    r = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, recompute=True)
+    assert torch.equal(s[2], r[2])
+    for a, b in zip(s[:2], r[:2]):
+        a, b = a.double(), b.double()
+        assert torch.isfinite(a).all()
+        assert ((a - b).norm() / b.norm()).item() < 4e-3
 
 
 # ---------------------------------------------------------------- log-prob / loss
