@@ -148,14 +148,14 @@ pp_status pp_attn_fwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv,
  * the input dtype; padding rows are written as 0.  The result is deterministic
  * (no atomics).  Errors as pp_attn_fwd.
  *
- * Workspace and mode: with ws_bytes >= pp_workspace_size's bwd, the key-major
- * pass stores dS (bf16, one value per query-key pair of every 32 x 32 block with
- * a visible pair, per query head) at the end of the workspace and the dQ pass
- * reads it back, so S, P and dP are computed once.  With ws_bytes between
- * pp_bwd_recompute_workspace_size's bwd and that, the dQ pass recomputes S and
- * dP instead (scratch linear in the tokens: Sec. 3.2.1's memory argument).
- * Both modes round dS to bf16 before the products that use it; they agree to
- * fp32 rounding.  Below the recompute size: PP_ERR_WORKSPACE_TOO_SMALL. */
+ * Workspace and mode: with ws_bytes >= pp_workspace_size's bwd the dQ pass
+ * recomputes S and dP (scratch linear in the tokens, as Sec. 3.2.1's memory
+ * argument assumes).  With ws_bytes >= pp_bwd_stored_ds_workspace_size's bwd
+ * the key-major pass also stores dS (bf16, one value per query-key pair of
+ * every 32 x 32 block with a visible pair, per query head) at the end of the
+ * workspace and the dQ pass reads it back instead, so S, P and dP are computed
+ * once.  Both modes round dS to bf16 before the products that use it; they agree
+ * to fp32 rounding.  Below pp_workspace_size's bwd: PP_ERR_WORKSPACE_TOO_SMALL. */
 pp_status pp_attn_bwd(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                       float scale, const void* q, const void* k, const void* v, const void* o,
                       const float* lse, const void* dout, void* dq, void* dk, void* dv, void* ws,
@@ -253,22 +253,22 @@ pp_status pp_attn_bwd_rope(const pp_pack_desc* desc, pp_dtype dtype, int hq, int
 typedef struct pp_plan pp_plan;
 
 /* Workspace bytes of a plan for this pack and shape (forward and backward
- * metadata and the backward's scratch, its stored dS included).  Errors as
+ * metadata and the backward's scratch, for the recompute backward).  Errors as
  * pp_attn_fwd. */
 pp_status pp_plan_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                                  size_t* bytes);
 
-/* The smaller workspaces that select the backward's recompute mode (see
+/* The larger workspaces that select the backward's stored-dS mode (see
  * pp_attn_bwd): *bwd for pp_attn_bwd / pp_attn_bwd_rope, *plan for
- * pp_plan_create (a plan made with less than pp_plan_workspace_size's bytes
- * runs its backward in that mode).  Either pointer may be NULL.  Errors as
- * pp_attn_fwd. */
-pp_status pp_bwd_recompute_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+ * pp_plan_create (a plan made with at least this many bytes stores dS).
+ * Either pointer may be NULL.  Errors as pp_attn_fwd, plus PP_ERR_UNSUPPORTED
+ * when the batch has 2^31 or more stored tiles per head. */
+pp_status pp_bwd_stored_ds_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                                           size_t* bwd, size_t* plan);
 
 /* Builds a plan and enqueues its metadata copy into ws (dev, ws_bytes >=
- * pp_plan_workspace_size's bytes, or >= pp_bwd_recompute_workspace_size's plan
- * for the recompute backward) on hip_stream.  rope_base (host, may be NULL)
+ * pp_plan_workspace_size's bytes, or >= pp_bwd_stored_ds_workspace_size's plan
+ * for the stored-dS backward) on hip_stream.  rope_base (host, may be NULL)
  * selects the rotary variants.  *plan receives the handle, or NULL on error.
  * Errors as pp_attn_fwd, plus PP_ERR_INVALID_ARGUMENT for a NULL plan pointer
  * or a bad rope_base. */

@@ -35,7 +35,7 @@ EXPORTED = [
     "pp_rope_workspace_size", "pp_rope", "pp_attn_fwd_rope", "pp_attn_bwd_rope",
     "pp_plan_workspace_size", "pp_plan_create", "pp_plan_destroy", "pp_attn_fwd_planned", "pp_attn_bwd_planned",
     "pp_attn_fwd_noalloc", "pp_build_id", "pp_logprob_row_count", "pp_seq_logprob_bwd_rows",
-    "pp_bwd_recompute_workspace_size",
+    "pp_bwd_stored_ds_workspace_size",
 ]
 
 NOALLOC_SCRATCH_BYTES = 4 << 20  # PP_NOALLOC_SCRATCH_BYTES
@@ -102,7 +102,7 @@ def lib() -> ctypes.CDLL:
     L.pp_attn_fwd_rope.argtypes = [D, i, i, i, i, f32, f32, P, P, P, P, P, P, P, P, sz, P]
     L.pp_attn_bwd_rope.argtypes = [D, i, i, i, i, f32, f32, P, P, P, P, P, P, P, P, P, P, sz, P]
     L.pp_plan_workspace_size.argtypes = [D, i, i, i, i, ctypes.POINTER(sz)]
-    L.pp_bwd_recompute_workspace_size.argtypes = [D, i, i, i, i, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    L.pp_bwd_stored_ds_workspace_size.argtypes = [D, i, i, i, i, ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.pp_plan_create.argtypes = [D, i, i, i, i, ctypes.POINTER(f32), P, sz, P, ctypes.POINTER(P)]
     L.pp_plan_destroy.argtypes = [P]
     L.pp_attn_fwd_planned.argtypes = [P, f32, P, P, P, P, P, P, P, P]
@@ -194,17 +194,17 @@ def pp_workspace_size(pack: Pack, hq: int = 1, hkv: int = 1, head_dim: int = 64,
     return tuple(int(v.value) if w else None for v, w in zip(vals, want))
 
 
-def pp_bwd_recompute_workspace_size(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16):
-    """(bwd, plan) workspace bytes that select the backward's recompute mode."""
+def pp_bwd_stored_ds_workspace_size(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16):
+    """(bwd, plan) workspace bytes that select the backward's stored-dS mode."""
     h = _DescHolder(pack)
     b, p = ctypes.c_size_t(0), ctypes.c_size_t(0)
-    _check(lib().pp_bwd_recompute_workspace_size(h.ref, dtype, hq, hkv, head_dim, ctypes.byref(b), ctypes.byref(p)))
+    _check(lib().pp_bwd_stored_ds_workspace_size(h.ref, dtype, hq, hkv, head_dim, ctypes.byref(b), ctypes.byref(p)))
     return int(b.value), int(p.value)
 
 
-def _bwd_workspace_bytes(pack: Pack, hq: int, hkv: int, d: int, dtype: int, recompute: bool) -> int:
-    if recompute:
-        return pp_bwd_recompute_workspace_size(pack, hq, hkv, d, dtype)[0]
+def _bwd_workspace_bytes(pack: Pack, hq: int, hkv: int, d: int, dtype: int, store_ds: bool) -> int:
+    if store_ds:
+        return pp_bwd_stored_ds_workspace_size(pack, hq, hkv, d, dtype)[0]
     return pp_workspace_size(pack, hq, hkv, d, fwd=False, bwd=True, loss=False, dtype=dtype)[1]
 
 
@@ -228,10 +228,10 @@ def pp_attn_fwd(pack: Pack, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, s
 
 
 def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, dk=None, dv=None,
-                ws=None, recompute: bool = False):
+                ws=None, store_ds: bool = False):
     """Packed attention backward; returns (dq, dk, dv) in the input dtype.  The
     library picks its mode from the workspace size: a workspace allocated here
-    holds the stored dS unless recompute is set."""
+    holds the stored dS when store_ds is set (else the dQ pass recomputes)."""
     T, hq, d = q.shape
     hkv = k.shape[1]
     h = _DescHolder(pack)
@@ -239,7 +239,7 @@ def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, 
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
     if ws is None:
-        ws = _workspace(_bwd_workspace_bytes(pack, hq, hkv, d, _dtype_code(q), recompute), q.device)
+        ws = _workspace(_bwd_workspace_bytes(pack, hq, hkv, d, _dtype_code(q), store_ds), q.device)
     _check(lib().pp_attn_bwd(h.ref, _dtype_code(q), hq, hkv, d, float(scale), _ptr(q), _ptr(k), _ptr(v),
                              _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),
                              ws.numel(), _stream(q.device)))
@@ -305,7 +305,7 @@ def pp_attn_fwd_rope(pack: Pack, q, k, v, rope_base: float, scale: float = 0.0, 
 
 
 def pp_attn_bwd_rope(pack: Pack, q_rot, k_rot, v, o, lse, dout, rope_base: float, scale: float = 0.0,
-                     dq=None, dk=None, dv=None, ws=None, recompute: bool = False):
+                     dq=None, dk=None, dv=None, ws=None, store_ds: bool = False):
     """Backward of pp_attn_fwd_rope: (dq, dk) with respect to the un-rotated q, k, and dv
     (workspace and mode as pp_attn_bwd)."""
     T, hq, d = q_rot.shape
@@ -315,7 +315,7 @@ def pp_attn_bwd_rope(pack: Pack, q_rot, k_rot, v, o, lse, dout, rope_base: float
     dk = torch.empty_like(k_rot) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
     if ws is None:
-        ws = _workspace(_bwd_workspace_bytes(pack, hq, hkv, d, _dtype_code(q_rot), recompute), q_rot.device)
+        ws = _workspace(_bwd_workspace_bytes(pack, hq, hkv, d, _dtype_code(q_rot), store_ds), q_rot.device)
     _check(lib().pp_attn_bwd_rope(h.ref, _dtype_code(q_rot), hq, hkv, d, float(scale), float(rope_base),
                                   _ptr(q_rot), _ptr(k_rot), _ptr(v), _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq),
                                   _ptr(dk), _ptr(dv), _ptr(ws), ws.numel(), _stream(q_rot.device)))
@@ -346,12 +346,12 @@ def pp_plan_workspace_size(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: 
 
 def pp_plan_create(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16,
                    rope_base: Optional[float] = None, ws: Optional[torch.Tensor] = None,
-                   device="cuda:0", recompute: bool = False) -> PlanHandle:
+                   device="cuda:0", store_ds: bool = False) -> PlanHandle:
     """Plans the pack once and stages the metadata into ws on the current stream
-    (a workspace allocated here holds the stored dS unless recompute is set)."""
+    (a workspace allocated here holds the stored dS when store_ds is set)."""
     h = _DescHolder(pack)
     if ws is None:
-        nb = (pp_bwd_recompute_workspace_size(pack, hq, hkv, head_dim, dtype)[1] if recompute
+        nb = (pp_bwd_stored_ds_workspace_size(pack, hq, hkv, head_dim, dtype)[1] if store_ds
               else pp_plan_workspace_size(pack, hq, hkv, head_dim, dtype))
         ws = _workspace(nb, device)
     base = ctypes.c_float(rope_base) if rope_base is not None else None

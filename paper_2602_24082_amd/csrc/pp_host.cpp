@@ -606,8 +606,8 @@ void plan_fwd(const Batch& bt, pp_dtype dtype, int hq, int hkv, int d, FwdPlan* 
 }
 
 // The backward's workspace ends with the stored-dS region (hq x ds_tiles
-// tiles of 32 x 32 bf16); a workspace that stops before it (lean_total bytes)
-// selects the recompute mode.
+// tiles of 32 x 32 bf16): a workspace that holds it (lay.total bytes) selects
+// the stored-dS mode, one that stops before it (lean_total) the recompute mode.
 struct BwdPlan {
   QPlan dq;
   std::vector<KTileItem> kv;
@@ -897,7 +897,7 @@ pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, in
   if (bwd) {
     BwdPlan p;
     plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
-    *bwd = p.lay.total;
+    *bwd = p.lean_total;  // the recompute mode; pp_bwd_stored_ds_workspace_size for the other
   }
   if (logprob) {
     if (vocab < 1) return fail(PP_ERR_INVALID_ARGUMENT, "vocab must be >= 1 for the logprob size");
@@ -1193,8 +1193,8 @@ pp_status attn_bwd_impl(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hk
   plan_bwd(bt, dtype, hq, hkv, head_dim, &p);
   if (ws_bytes < p.lean_total)
     return fail(PP_ERR_WORKSPACE_TOO_SMALL,
-                "backward needs %zu workspace bytes (%zu without the stored dS), got %zu", p.lay.total,
-                p.lean_total, ws_bytes);
+                "backward needs %zu workspace bytes (%zu with the stored dS), got %zu", p.lean_total,
+                p.lay.total, ws_bytes);
   const bool store_ds = p.ds_tiles >= 0 && ws_bytes >= p.lay.total;
   if (p.lean_total && !ws) return fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
   if (ws && !aligned256(ws)) return fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");
@@ -1283,18 +1283,20 @@ pp_status pp_plan_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int h
   pp_plan p{};
   pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, nullptr, &bt, &p);
   if (st != PP_OK) return st;
-  *bytes = p.bwd_off + p.bwd.lay.total;
+  *bytes = p.bwd_off + p.bwd.lean_total;
   return PP_OK;
 }
 
-pp_status pp_bwd_recompute_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
+pp_status pp_bwd_stored_ds_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                                           size_t* bwd, size_t* plan) {
   Batch bt;
   pp_plan p{};
   pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, nullptr, &bt, &p);
   if (st != PP_OK) return st;
-  if (bwd) *bwd = p.bwd.lean_total;
-  if (plan) *plan = p.bwd_off + p.bwd.lean_total;
+  if (p.bwd.ds_tiles < 0)
+    return fail(PP_ERR_UNSUPPORTED, "the stored dS of this batch does not fit 32-bit tile offsets");
+  if (bwd) *bwd = p.bwd.lay.total;
+  if (plan) *plan = p.bwd_off + p.bwd.lay.total;
   return PP_OK;
 }
 
@@ -1308,8 +1310,8 @@ pp_status pp_plan_create(const pp_pack_desc* desc, pp_dtype dtype, int hq, int h
   pp_status st = plan_common(desc, dtype, hq, hkv, head_dim, rope_base, &bt, p);
   const size_t total = p->bwd_off + p->bwd.lay.total, lean = p->bwd_off + p->bwd.lean_total;
   if (st == PP_OK && ws_bytes < lean)
-    st = fail(PP_ERR_WORKSPACE_TOO_SMALL, "the plan needs %zu workspace bytes (%zu without the stored dS), got %zu",
-              total, lean, ws_bytes);
+    st = fail(PP_ERR_WORKSPACE_TOO_SMALL, "the plan needs %zu workspace bytes (%zu with the stored dS), got %zu",
+              lean, total, ws_bytes);
   p->store_ds = p->bwd.ds_tiles >= 0 && ws_bytes >= total;
   if (st == PP_OK && lean && !ws) st = fail(PP_ERR_INVALID_ARGUMENT, "ws is NULL");
   if (st == PP_OK && ws && !aligned256(ws)) st = fail(PP_ERR_INVALID_ARGUMENT, "ws must be 256-byte aligned");

@@ -382,8 +382,8 @@ def test_noalloc_forward_rejects_packs_beyond_its_static_scratch():
 
 
 def test_stored_ds_region_is_one_tile_per_visible_block_and_head():
-    """The backward's stored-dS region -- the difference between its workspace
-    and the recompute mode's -- holds one 32 x 32 bf16 tile (2 KB) per query head
+    """The backward's stored-dS region -- the difference between the stored-dS
+    mode's workspace and the default one -- holds one 32 x 32 bf16 tile (2 KB) per query head
     for every 32 x 32 block of a row's mask that has a visible pair (the
     oracle's dense mask), and nothing more: the visible queries of 32
     consecutive keys form one run from the block's diagonal, which is what the
@@ -395,16 +395,16 @@ def test_stored_ds_region_is_one_tile_per_visible_block_and_head():
     for pack in packs:
         n_blocks = int((orc.pack_tile_classes(*pack.oracle_args(), 32, 32) > 0).sum())
         for hq, hkv in ((4, 2), (3, 1)):
-            full = binding.pp_workspace_size(pack, hq, hkv, 64, fwd=False, bwd=True, loss=False)[1]
-            lean, plan_lean = binding.pp_bwd_recompute_workspace_size(pack, hq, hkv, 64)
+            lean = binding.pp_workspace_size(pack, hq, hkv, 64, fwd=False, bwd=True, loss=False)[1]
+            full, plan_full = binding.pp_bwd_stored_ds_workspace_size(pack, hq, hkv, 64)
             assert full - lean == hq * n_blocks * 2048
-            assert binding.pp_plan_workspace_size(pack, hq, hkv, 64) - plan_lean == hq * n_blocks * 2048
+            assert plan_full - binding.pp_plan_workspace_size(pack, hq, hkv, 64) == hq * n_blocks * 2048
 
 
 def test_backward_below_the_recompute_workspace_is_refused():
     pack = wl.make_pack([50], [[20, 30]])
-    lean, _ = binding.pp_bwd_recompute_workspace_size(pack, 2, 1, 64)
-    full = binding.pp_workspace_size(pack, 2, 1, 64, fwd=False, bwd=True, loss=False)[1]
+    lean = binding.pp_workspace_size(pack, 2, 1, 64, fwd=False, bwd=True, loss=False)[1]
+    full, _ = binding.pp_bwd_stored_ds_workspace_size(pack, 2, 1, 64)
     assert 0 < lean < full
     L = binding.lib()
     h = binding._DescHolder(pack)
@@ -412,4 +412,4 @@ def test_backward_below_the_recompute_workspace_is_refused():
     st = L.pp_attn_bwd(h.ref, binding.PP_BF16, 2, 1, 64, 0.0, fake, fake, fake, fake, fake, fake, fake, fake,
                        fake, fake, lean - 1, None)
     assert binding.STATUS[st] == "PP_ERR_WORKSPACE_TOO_SMALL"
-    assert b"without the stored dS" in L.pp_last_error()
+    assert b"with the stored dS" in L.pp_last_error()

@@ -43,21 +43,21 @@ def _pick_row(pack, which):
     return int(np.argsort(n, kind="stable")[len(n) // 2])  # median length
 
 
-def _attention_sample(cfg_index, group, which):
+def _attention_sample(cfg_index, group, which, store_ds=False):
     cfg = wl.CONFIGS[cfg_index]
     pack = wl.config_pack(cfg)
     seed = wl.tensor_seed(cfg.index, 0)
     q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, seed, torch.bfloat16, DEV)
     o, lse = pp.pp_attn_fwd(pack, q, k, v)
-    dq, dk, dv = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
+    dq, dk, dv = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, store_ds=store_ds)
     torch.cuda.synchronize()
     b = _pick_row(pack, which)
     r0, r1 = int(pack.row_start[b]), int(pack.row_start[b + 1])
     G = cfg.hq // cfg.hkv
     hs = slice(group * G, (group + 1) * G)
     gs = slice(group, group + 1)
-    print(f"{cfg.name}: {which} row {b} T={r1 - r0}, q-heads {hs.start}..{hs.stop - 1}, kv-head {group}",
-          flush=True)
+    print(f"{cfg.name}: {which} row {b} T={r1 - r0}, q-heads {hs.start}..{hs.stop - 1}, kv-head {group}"
+          f" store_ds={store_ds}", flush=True)
     sub = lambda x, s: x[r0:r1, s].double().cpu().numpy()
     row = _row_pack(pack, b)
     args = row.oracle_args()
@@ -94,6 +94,12 @@ def test_fullsize_long_prefix_attention(which):
 @pytest.mark.parametrize("which", ["longest", "shortest"])
 def test_fullsize_dpo_chain_attention(which):
     _attention_sample(4, group=0, which=which)
+
+
+@pytest.mark.parametrize("cfg_index,group,which", [(1, 6, "longest"), (3, 2, "median"), (4, 5, "longest")])
+def test_fullsize_attention_stored_ds(cfg_index, group, which):
+    """The stored-dS backward on whole benchmarked batches (0.45 to 12 GB of dS)."""
+    _attention_sample(cfg_index, group=group, which=which, store_ds=True)
 
 
 def _attention_rope_sample(cfg_index, group, base):

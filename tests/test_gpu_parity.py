@@ -39,11 +39,12 @@ def _poisoned_like(t):
 
 
 def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None, grads=("dq", "dk", "dv"),
-                     recompute=False):
-    """Forward and backward against the oracle; recompute selects the backward
-    mode that recomputes S and dP in the dQ pass instead of reading stored dS."""
+                     store_ds=False):
+    """Forward and backward against the oracle; store_ds selects the backward
+    mode whose dQ pass reads the dS stored by the key-major pass instead of
+    recomputing S and dP."""
     print(f"case rows={pack.num_rows} T={pack.total_tokens} hq={hq} hkv={hkv} d={d} {dtype} seed={seed}"
-          f" recompute={recompute}", flush=True)
+          f" store_ds={store_ds}", flush=True)
     q, k, v, do = _inputs(pack, hq, hkv, d, dtype, seed) if inputs is None else inputs
     qg, kg, vg, dog = (x.to(DEV) for x in (q, k, v, do))
     T = pack.total_tokens
@@ -64,7 +65,7 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
     if not check_bwd:
         return
     dq, dk, dv = _poisoned_like(qg), _poisoned_like(kg), _poisoned_like(vg)
-    pp.pp_attn_bwd(pack, qg, kg, vg, o, lse, dog, dq=dq, dk=dk, dv=dv, recompute=recompute)
+    pp.pp_attn_bwd(pack, qg, kg, vg, o, lse, dog, dq=dq, dk=dk, dv=dv, store_ds=store_ds)
     dq_r, dk_r, dv_r = orc.attn_bwd(*args, qn, kn, vn, don)
     out = {}
     for name, got, ref in (("dq", dq, dq_r), ("dk", dk, dk_r), ("dv", dv, dv_r)):
@@ -85,20 +86,20 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
     return out
 
 
-@pytest.mark.parametrize("recompute", [False, True])
-def test_tiny_fp32_config(recompute):
+@pytest.mark.parametrize("store_ds", [False, True])
+def test_tiny_fp32_config(store_ds):
     """4 rows, 4 heads (MHA), d 64, fp32 inputs, K=2 (the tiny check config)."""
     cfg = wl.CONFIGS[0]
-    _check_attention(wl.config_pack(cfg), cfg.hq, cfg.hkv, cfg.head_dim, torch.float32, 11, recompute=recompute)
+    _check_attention(wl.config_pack(cfg), cfg.hq, cfg.hkv, cfg.head_dim, torch.float32, 11, store_ds=store_ds)
 
 
-@pytest.mark.parametrize("recompute", [False, True])
+@pytest.mark.parametrize("store_ds", [False, True])
 @pytest.mark.parametrize("d", [64, 128])
-def test_bf16_gqa_ragged(d, recompute):
+def test_bf16_gqa_ragged(d, store_ds):
     """Several tiles per row, unaligned boundaries, padding, GQA 8/2."""
     pack = wl.make_pack([300, 0, 129, 5, 64], [[70, 45], [33, 64], [1, 0, 200], [130], [64, 64]],
                         pad=[3, 0, 0, 17, 0])
-    _check_attention(pack, 8, 2, d, torch.bfloat16, 21 + d, recompute=recompute)
+    _check_attention(pack, 8, 2, d, torch.bfloat16, 21 + d, store_ds=store_ds)
 
 
 def test_bf16_k4_mha():
@@ -106,16 +107,16 @@ def test_bf16_k4_mha():
     _check_attention(pack, 4, 4, 128, torch.bfloat16, 31)
 
 
-@pytest.mark.parametrize("recompute", [False, True])
-def test_edge_cases(recompute):
+@pytest.mark.parametrize("store_ds", [False, True])
+def test_edge_cases(store_ds):
     """Single response (plain causal), empty prompt (document masking), one-token
     rows, empty rows, all-padding rows, rows shorter than one tile."""
     pack = wl.make_pack([0, 1, 7, 0, 129, 3, 0],
                         [[1], [], [0, 0], [], [], [1, 1, 1], [5, 6]],
                         pad=[0, 0, 0, 0, 0, 2, 0])
-    _check_attention(pack, 4, 1, 64, torch.bfloat16, 41, recompute=recompute)
+    _check_attention(pack, 4, 1, 64, torch.bfloat16, 41, store_ds=store_ds)
     pack = wl.make_pack([5, 0], [[], []], pad=[0, 9])  # all-padding second row
-    _check_attention(pack, 2, 2, 128, torch.bfloat16, 42, recompute=recompute)
+    _check_attention(pack, 2, 2, 128, torch.bfloat16, 42, store_ds=store_ds)
 
 
 @pytest.mark.parametrize("seed", range(8))
@@ -123,7 +124,7 @@ def test_random_pack_sweep(seed):
     """Seeded random packs: prompt lengths 0-400 (the first row has none on two
     seeds: its responses are then separate documents), 0-4 responses of 0-260
     tokens, 0-20 padding tokens, GQA ratios 1, 2, 4 and 8, d 64 or 128; forward
-    and all three gradients against the oracle (odd seeds: the recompute
+    and all three gradients against the oracle (odd seeds: the stored-dS
     backward)."""
     rng = np.random.default_rng(1000 + seed)
     B = int(rng.integers(1, 5))
@@ -141,7 +142,7 @@ def test_random_pack_sweep(seed):
     hkv = int(rng.choice([1, 2, 4]))
     G = int(rng.choice([1, 2, 4, 8]))
     d = int(rng.choice([64, 128]))
-    _check_attention(pack, hkv * G, hkv, d, torch.bfloat16, 2000 + seed, recompute=bool(seed % 2))
+    _check_attention(pack, hkv * G, hkv, d, torch.bfloat16, 2000 + seed, store_ds=bool(seed % 2))
 
 
 def test_large_scores():
@@ -218,13 +219,13 @@ def test_g8_long_prefix_small():
     _check_attention(pack, 16, 2, 128, torch.bfloat16, 51)
 
 
-@pytest.mark.parametrize("recompute", [False, True])
-def test_backward_is_deterministic(recompute):
+@pytest.mark.parametrize("store_ds", [False, True])
+def test_backward_is_deterministic(store_ds):
     pack = wl.make_pack([400, 150], [[100, 61], [33, 270]])
     q, k, v, do = (x.to(DEV) for x in _inputs(pack, 8, 2, 128, torch.bfloat16, 61))
     o, lse = pp.pp_attn_fwd(pack, q, k, v)
-    g1 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, recompute=recompute)
-    g2 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, recompute=recompute)
+    g1 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, store_ds=store_ds)
+    g2 = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, store_ds=store_ds)
     o2, lse2 = pp.pp_attn_fwd(pack, q, k, v)
     assert torch.equal(o, o2) and torch.equal(lse, lse2)
     for a, b in zip(g1, g2):
@@ -238,8 +239,8 @@ def test_stored_and_recompute_backward_agree():
     pack = wl.make_pack([333, 90, 0], [[129, 64, 1, 40], [300], [65, 31]], pad=[5, 0, 11])
     q, k, v, do = (x.to(DEV) for x in _inputs(pack, 8, 2, 128, torch.bfloat16, 71))
     o, lse = pp.pp_attn_fwd(pack, q, k, v)
-    s = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
-    r = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, recompute=True)
+    s = pp.pp_attn_bwd(pack, q, k, v, o, lse, do, store_ds=True)
+    r = pp.pp_attn_bwd(pack, q, k, v, o, lse, do)
     assert torch.equal(s[2], r[2])
     for a, b in zip(s[:2], r[:2]):
         a, b = a.double(), b.double()

@@ -29,22 +29,22 @@ def _ragged():
                         pad=[3, 0, 0, 17, 0])
 
 
-@pytest.mark.parametrize("dtype,d,hq,hkv,recompute", [(torch.bfloat16, 128, 8, 2, False),
+@pytest.mark.parametrize("dtype,d,hq,hkv,store_ds", [(torch.bfloat16, 128, 8, 2, False),
                                                       (torch.bfloat16, 64, 4, 4, False),
                                                       (torch.float32, 64, 4, 2, False),
                                                       (torch.bfloat16, 128, 8, 2, True)])
-def test_planned_equals_self_contained(dtype, d, hq, hkv, recompute):
-    """A plan made with the smaller workspace runs the recompute backward, as the
-    self-contained call does with its smaller workspace."""
+def test_planned_equals_self_contained(dtype, d, hq, hkv, store_ds):
+    """A plan made with the larger workspace runs the stored-dS backward, as the
+    self-contained call does with its larger workspace."""
     pack = _ragged()
-    print(f"case plan T={pack.total_tokens} d={d} hq={hq} hkv={hkv} {dtype} recompute={recompute}", flush=True)
+    print(f"case plan T={pack.total_tokens} d={d} hq={hq} hkv={hkv} {dtype} store_ds={store_ds}", flush=True)
     code = pp.PP_FP32 if dtype == torch.float32 else pp.PP_BF16
-    plan = pp.pp_plan_create(pack, hq, hkv, d, dtype=code, device=DEV, recompute=recompute)
+    plan = pp.pp_plan_create(pack, hq, hkv, d, dtype=code, device=DEV, store_ds=store_ds)
     for layer in range(3):
         q, k, v, do = wl.qkv(pack, hq, hkv, d, 300 + layer, dtype, device=DEV)
         o1, l1 = pp.pp_attn_fwd(pack, q, k, v)
         o2, l2 = pp.pp_attn_fwd_planned(plan, q, k, v)
-        g1 = pp.pp_attn_bwd(pack, q, k, v, o1, l1, do, recompute=recompute)
+        g1 = pp.pp_attn_bwd(pack, q, k, v, o1, l1, do, store_ds=store_ds)
         g2 = pp.pp_attn_bwd_planned(plan, q, k, v, o2, l2, do)
         torch.cuda.synchronize()
         assert torch.equal(o1, o2) and torch.equal(l1, l2), layer
