@@ -98,9 +98,10 @@ def logit_rows_needed(pack: wl.Pack) -> int:
 
 
 class Attn:
-    """Inputs, outputs and workspaces of one attention fwd+bwd on a pack."""
+    """Inputs, outputs and workspaces of one attention fwd+bwd on a pack; with
+    store_ds the backward's workspace holds the stored dS (its other mode)."""
 
-    def __init__(self, pack, hq, hkv, d, seed, dev):
+    def __init__(self, pack, hq, hkv, d, seed, dev, store_ds=False):
         self.pack = pack
         self.q, self.k, self.v, self.do = wl.qkv(pack, hq, hkv, d, seed, torch.bfloat16, dev)
         T = pack.total_tokens
@@ -110,6 +111,8 @@ class Attn:
         self.dk = torch.empty_like(self.k)
         self.dv = torch.empty_like(self.v)
         f, b, _, _ = pp.pp_workspace_size(pack, hq, hkv, d, fwd=True, bwd=True, loss=False)
+        if store_ds:
+            b = pp.pp_bwd_stored_ds_workspace_size(pack, hq, hkv, d)[0]
         self.ws_f = torch.empty(max(f, 1), dtype=torch.uint8, device=dev)
         self.ws_b = torch.empty(max(b, 1), dtype=torch.uint8, device=dev)
 
@@ -144,8 +147,8 @@ def median_time(fn, iters=10, warmup=3, reps=5):
     return float(np.median(times))
 
 
-def time_attention(pack, hq, hkv, d, dev, iters=10, warmup=3):
-    a = Attn(pack, hq, hkv, d, 977, dev)
+def time_attention(pack, hq, hkv, d, dev, iters=10, warmup=3, store_ds=False):
+    a = Attn(pack, hq, hkv, d, 977, dev, store_ds=store_ds)
     ms = median_time(a.run, iters, warmup)
     del a
     torch.cuda.empty_cache()
@@ -226,7 +229,7 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def attention_memory(pack, hq, hkv, d, dev):
+def attention_memory(pack, hq, hkv, d, dev, store_ds=False):
     """Device memory of one attention fwd+bwd on a layout: the allocator's
     high-water mark above what was allocated before, with q, k, v, dO, the
     outputs O and LSE, the gradients and both workspaces live (the library
@@ -236,7 +239,7 @@ def attention_memory(pack, hq, hkv, d, dev):
     torch.cuda.empty_cache()
     base = torch.cuda.memory_allocated(dev)
     torch.cuda.reset_peak_memory_stats(dev)
-    a = Attn(pack, hq, hkv, d, 977, dev)
+    a = Attn(pack, hq, hkv, d, 977, dev, store_ds=store_ds)
     a.run()
     torch.cuda.synchronize()
     peak = torch.cuda.max_memory_allocated(dev) - base
@@ -262,16 +265,20 @@ def memory_leg(pack, hq, hkv, d, dev):
             out["packed"]["activation_bytes"] / out[name]["activation_bytes"], 4)
     out["tokens_packed_over_unpacked"] = round(st["tokens_packed"] / st["tokens_unpacked"], 4)
     out["eq1_memory_ratio"] = round(st["eq1_memory_ratio"], 4)
+    # the backward's other mode keeps dS (one bf16 per pair of each visible
+    # 32 x 32 block, per head): memory then follows pairs, not tokens
+    peak, _ = attention_memory(pack, hq, hkv, d, dev, store_ds=True)
+    out["packed_stored_ds_peak_bytes"] = peak
     out["measured_by"] = ("torch.cuda.max_memory_allocated over one attention fwd+bwd (inputs, dO, O, LSE, "
-                          "gradients, workspaces)")
+                          "gradients, workspaces; the default backward, which recomputes S and dP in its dQ pass)")
     return out
 
 
-def attention_kernels(pack, hq, hkv, d, dev, iters=5):
+def attention_kernels(pack, hq, hkv, d, dev, iters=5, store_ds=False):
     """Per-kernel average launch times of attention fwd+bwd on a pack (library
     events around every launch) and each kernel's fraction of the bf16 peak on
     its useful work."""
-    a = Attn(pack, hq, hkv, d, 977, dev)
+    a = Attn(pack, hq, hkv, d, 977, dev, store_ds=store_ds)
     for _ in range(2):
         a.run()
     torch.cuda.synchronize()
@@ -293,11 +300,36 @@ def attention_kernels(pack, hq, hkv, d, dev, iters=5):
             ms = kt[k][0] / kt[k][1]
             ach = units * d * hq * U / (ms * 1e-3) / 1e12
             out[k] = {"avg_ms": round(ms, 4), "useful_TFLOP_s": round(ach, 1), "frac": round(ach / PEAK_BF16_TFLOPS, 4)}
-    bwd_ms = sum(kt[k][0] / kt[k][1] for k in ("pp_attn_bwd_dkdv", "pp_attn_bwd_dq") if k in kt)
+    if "pp_attn_bwd_prep" in kt:
+        out["pp_attn_bwd_prep"] = {"avg_ms": round(kt["pp_attn_bwd_prep"][0] / kt["pp_attn_bwd_prep"][1], 4)}
+    bwd_k = ("pp_attn_bwd_prep", "pp_attn_bwd_dkdv", "pp_attn_bwd_dq")
+    bwd_ms = sum(kt[k][0] / kt[k][1] for k in bwd_k if k in kt)
     if bwd_ms > 0:
         ach = 10 * d * hq * U / (bwd_ms * 1e-3) / 1e12
         out["backward_10_units"] = {"ms": round(bwd_ms, 4), "useful_TFLOP_s": round(ach, 1),
-                                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "rule": "over the dQ and dK/dV kernels"}
+                                    "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                                    "rule": "over the backward's kernels (delta pre-pass when present, dK/dV, dQ)"}
+    return out
+
+
+def stored_ds_leg(pack, hq, hkv, d, dev, with_kernels=True):
+    """The backward's other mode: dK/dV stores dS and the dQ pass reads it back
+    instead of recomputing S and dP.  Attention fwd+bwd time against the
+    default mode (timed alternately), the dS bytes and the kernels."""
+    U = useful_pairs(pack)
+    lean = pp.pp_workspace_size(pack, hq, hkv, d, fwd=False, bwd=True, loss=False)[1]
+    full = pp.pp_bwd_stored_ds_workspace_size(pack, hq, hkv, d)[0]
+    t_s, t_r = [], []
+    for _ in range(2):
+        t_r.append(time_attention(pack, hq, hkv, d, dev, iters=5, warmup=2))
+        t_s.append(time_attention(pack, hq, hkv, d, dev, iters=5, warmup=2, store_ds=True))
+    ts, tr = min(t_s), min(t_r)
+    out = {"attn_fwd_bwd_ms": round(ts, 4), "useful_TFLOP_s": round(14 * d * hq * U / (ts * 1e-3) / 1e12, 1),
+           "recompute_mode_ms": round(tr, 4), "speedup_over_recompute_mode": round(tr / ts, 4),
+           "ds_bytes": int(full - lean), "bwd_workspace_bytes": int(full),
+           "rule": "best of two alternating runs of each mode"}
+    if with_kernels:
+        out["kernels"] = attention_kernels(pack, hq, hkv, d, dev, store_ds=True)
     return out
 
 
@@ -316,7 +348,8 @@ def workload_leg(cfg_index, dev):
             "attn_fwd_bwd_ms": round(t, 4), "useful_TFLOP_s": round(tf, 1),
             "pct_bf16_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
             "unpacked_padded_ms": round(t_pad, 4), "speedup_vs_padded": round(t_pad / t, 3),
-            "kernels": attention_kernels(pack, hq, hkv, d, dev)}
+            "kernels": attention_kernels(pack, hq, hkv, d, dev),
+            "stored_ds": stored_ds_leg(pack, hq, hkv, d, dev, with_kernels=False)}
 
 
 def chain_sorting(dev, reps=1):
@@ -516,6 +549,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--prewarm-s", type=float, default=2.0,
+                    help="untimed steps for this many seconds before the warm-up steps: the first GPU "
+                         "process on a fresh machine otherwise times some steps before the clocks settle")
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
@@ -594,6 +630,14 @@ def main():
         "pp_logprob_rows": ("hbm", n_rows * V * 2 + n_rows * 16),
     }
 
+    t_pre = time.perf_counter()
+    n_pre = 0
+    while time.perf_counter() - t_pre < args.prewarm_s:
+        step(False)
+        n_pre += 1
+        if n_pre % 50 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
     for _ in range(args.warmup):
         step(False)
     # per-kernel breakdown: a short pass with every launch between hipEvents picks
@@ -755,12 +799,13 @@ def main():
         losing = {"workload": "8 rows, prompt 32-96, K=2 responses 768-1024 (responses >> prompt)",
                   **losing[0], **losing[1]}
 
-    memory = workloads = chain = None
+    memory = workloads = chain = stored = None
     if not args.no_extra:
         # free the step's large buffers first: the other legs allocate their own
         del logits_pol, logits_ref, attn
         torch.cuda.empty_cache()
         memory = memory_leg(pack, hq, cfg.hkv, d, dev)
+        stored = stored_ds_leg(pack, hq, cfg.hkv, d, dev)
         workloads = {wl.CONFIGS[i].name: workload_leg(i, dev) for i in (2, 3, 4) if i != args.config}
         chain = chain_sorting(dev)
 
@@ -778,6 +823,8 @@ def main():
         "ms_per_step": round(ms_step, 4),
         "attn_ms_per_step": round(attn_ms, 4),
         "attn_ms_median_step": round(float(np.median(attn_each)), 4),
+        "attn_ms_steps": [round(x, 4) for x in attn_each],
+        "prewarm": {"seconds": args.prewarm_s, "steps": n_pre},
         "pct_bf16_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "higher_is_better": True,
         "scaling": "weak",
@@ -802,6 +849,7 @@ def main():
         "kernels": kernels,
         "kernel_breakdown_steps": n_breakdown,
         "attention_rooflines": attn_roofs,
+        "stored_ds_backward": stored,
         "roofline": roof,
         "cpu_baseline": cpu,
         "loss": loss_val,
