@@ -557,6 +557,10 @@ def main():
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
     ap.add_argument("--chain-sorting", action="store_true", help="print only the DPO chain leg")
+    ap.add_argument("--attn-loop", type=int, default=0,
+                    help="profiling mode: run only N attention fwd+bwd passes on --config's batch "
+                         "(default backward mode; --store-ds for the other) and print their mean time")
+    ap.add_argument("--store-ds", action="store_true", help="with --attn-loop: the stored-dS backward")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the other workloads, the measured memory and the DPO chain")
     args = ap.parse_args()
@@ -573,6 +577,13 @@ def main():
         return
     if args.chain_sorting:
         print(json.dumps(chain_sorting(dev)))
+        return
+    if args.attn_loop:
+        cfg = wl.CONFIGS[args.config]
+        pack = wl.config_pack(cfg)
+        ms = time_attention(pack, cfg.hq, cfg.hkv, cfg.head_dim, dev, iters=args.attn_loop, warmup=2,
+                            store_ds=args.store_ds)
+        print(json.dumps({"workload": cfg.name, "store_ds": args.store_ds, "attn_fwd_bwd_ms": round(ms, 4)}))
         return
 
     cfg = wl.CONFIGS[args.config]
