@@ -75,9 +75,9 @@ def test_rope_standalone(dtype, name, mk, d, base):
     _check_rot(back, ref_back, np.abs(xn).max(), dtype == torch.bfloat16)
 
 
-def _check_fused(pack, hq, hkv, d, base, dtype, seed):
-    print(f"case attn_rope T={pack.total_tokens} hq={hq} hkv={hkv} d={d} base={base} {dtype} seed={seed}",
-          flush=True)
+def _check_fused(pack, hq, hkv, d, base, dtype, seed, store_ds=False):
+    print(f"case attn_rope T={pack.total_tokens} hq={hq} hkv={hkv} d={d} base={base} {dtype} seed={seed}"
+          f" store_ds={store_ds}", flush=True)
     q, k, v, do = wl.qkv(pack, hq, hkv, d, seed, dtype, device="cpu")
     qg, kg, vg, dog = (x.to(DEV) for x in (q, k, v, do))
     o, lse, q_rot, k_rot = pp.pp_attn_fwd_rope(pack, qg, kg, vg, base)
@@ -98,7 +98,7 @@ def _check_fused(pack, hq, hkv, d, base, dtype, seed):
     bf = dtype == torch.bfloat16
     _check_rot(q_rot, qr_ref, np.abs(qn).max(), bf)
     _check_rot(k_rot, kr_ref, np.abs(kn).max(), bf)
-    dq, dk, dv = pp.pp_attn_bwd_rope(pack, q_rot, k_rot, vg, o, lse, dog, base)
+    dq, dk, dv = pp.pp_attn_bwd_rope(pack, q_rot, k_rot, vg, o, lse, dog, base, store_ds=store_ds)
     dqr, dkr, dv_r = orc.attn_bwd(*args, qr_b, kr_b, vn, don)
     dq_r = orc.pack_rope(*args, dqr, base, inverse=True)
     dk_r = orc.pack_rope(*args, dkr, base, inverse=True)
@@ -109,11 +109,13 @@ def _check_fused(pack, hq, hkv, d, base, dtype, seed):
     return (qg, kg, vg, dog), (o, lse, q_rot, k_rot), (dq, dk, dv)
 
 
+@pytest.mark.parametrize("store_ds", [False, True])
 @pytest.mark.parametrize("d,hq,hkv", [(128, 8, 2), (64, 4, 4)])
-def test_fused_rope_attention_matches_oracle(d, hq, hkv):
+def test_fused_rope_attention_matches_oracle(d, hq, hkv, store_ds):
+    """Both backward modes: the stored-dS dQ pass rotates its gradient back too."""
     pack = wl.make_pack([300, 0, 129, 5, 64], [[70, 45], [33, 64], [1, 0, 200], [130], [64, 64]],
                         pad=[3, 0, 0, 17, 0])
-    _check_fused(pack, hq, hkv, d, 500000.0, torch.bfloat16, 77)
+    _check_fused(pack, hq, hkv, d, 500000.0, torch.bfloat16, 77, store_ds=store_ds)
 
 
 def test_fused_rope_attention_fp32_tiny_config():
