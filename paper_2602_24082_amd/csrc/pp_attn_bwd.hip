@@ -424,6 +424,11 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
   constexpr int RPW = QBN / NW;
   using Dma = TileDma<D, RPW>;
   __shared__ __attribute__((aligned(1024))) __bf16 sKV[NS][2][QBN * D];
+  // each lane's hole length, read back only on blocks of the general masked
+  // class: kept out of registers, which are all taken, because the spill
+  // reload the compiler otherwise placed there waited (vmcnt) for the next
+  // tile's DMA as well
+  __shared__ unsigned s_hole[NW][64];
 
   int item_idx, head;
   item_and_head(blockIdx.x, p.hq, item_idx, head);
@@ -441,8 +446,11 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
   const bool in_tile = i < it.q_end;
   const bool real = i < it.valid;
   const int hi = real ? i : -1;
-  const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
-  const unsigned hole = (real && lo > it.P) ? (unsigned)(lo - it.P) : 0u;
+  {
+    const int lo = real ? p.seg_lo[it.tok0 + i] : 0;
+    // this wave's own entries: read back by the same wave, after this store
+    s_hole[wave][lane] = (real && lo > it.P) ? (unsigned)(lo - it.P) : 0u;
+  }
   const int64_t qrow = (int64_t)(it.tok0 + i) * p.hq + head;
   bf16x8 qf[D / 16], df[D / 16];
 #pragma unroll
@@ -553,7 +561,7 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
       // is not in the hole [P, lo), i.e. off not in [P - k0 - 4hf, + hole)
       const int lim = hi - k0 - 4 * hf;
       const int h0 = it.P - k0 - 4 * hf;
-      const int hn = cls == kWaveMasked ? (int)hole : 0;
+      const int hn = cls == kWaveMasked ? (int)s_hole[wave][lane_id_here()] : 0;
       const uint64_t vis = bits_below64(lim + 1) & ~(bits_below64(h0 + hn) & ~bits_below64(h0));
       const uint32_t vis_lo = (uint32_t)vis, vis_hi = (uint32_t)(vis >> 32);
 #pragma unroll

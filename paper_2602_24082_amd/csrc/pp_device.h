@@ -237,6 +237,16 @@ __device__ __forceinline__ bf16x8 lds_tr8_tile32(const __bf16* tile, int row16, 
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// The lane's index in its wave, formed where it is used (v_mbcnt from no
+// input register; volatile, so the compiler neither hoists it out of a loop
+// nor keeps it live across one -- under full register pressure it spilled
+// such a value and reloaded it with a wait that also covered the tile DMAs).
+__device__ __forceinline__ int lane_id_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // Workgroup barrier that orders LDS accesses only (s_waitcnt lgkmcnt(0);
 // s_barrier): global stores issued before it stay in flight, where
 // __syncthreads would wait for them.  LDS filled by DMA is published by an
