@@ -510,6 +510,9 @@ __global__ __launch_bounds__(NW * 64, PP_DQ_MIN_WAVES) void bwd_dq_kernel(BwdPar
   for (int m = 0; m < D / 32; ++m) acc[m] = f32x16{};
 
   for (int t = 0; t < n_tiles; ++t) {
+    // a scalar load per tile: a VGPR copy of the tile list read with
+    // v_readlane costs this kernel, already at 256 registers, spill reloads
+    // inside the loop
     const KTileEntry e = load_uniform(ktiles + t);
     const int k0 = e.k0;
     const int cls = tile_wave_class(e.cls, wave);
