@@ -531,7 +531,7 @@ def pp_pack_stats(pack: Pack) -> dict:
 def pp_pack_export(pack: Pack, block_q: int = 128, block_k: int = 64, tiles: bool = True):
     """Host-only integer export: (position_ids, segment_ids, tile_class) numpy arrays."""
     h = _DescHolder(pack)
-    T = pack.total_tokens
+    T = max(0, pack.total_tokens)  # a broken descriptor is the library's to report
     pos = np.zeros(T, np.int32)
     seg = np.zeros(T, np.int32)
     n = ctypes.c_size_t(0)
