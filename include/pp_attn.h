@@ -116,8 +116,10 @@ typedef struct pp_pack_desc {
  * Any output pointer may be NULL.  dtype is the attention input dtype (fp32
  * inputs need room for their bf16 copies).  vocab is used only for logprob and
  * may be 0.  hq, hkv and head_dim are validated as for pp_attn_fwd when fwd or
- * bwd is requested.  logprob serves both pp_seq_logprob and pp_seq_logprob_bwd.
- * loss is the workspace of pp_dpo_loss for this batch's B. */
+ * bwd is requested.  bwd is the workspace of pp_attn_bwd / pp_attn_bwd_rope in
+ * their default (recompute) mode; pp_bwd_stored_ds_workspace_size gives the
+ * larger one of the stored-dS mode.  logprob serves both pp_seq_logprob and
+ * pp_seq_logprob_bwd.  loss is the workspace of pp_dpo_loss for this batch's B. */
 pp_status pp_workspace_size(const pp_pack_desc* desc, pp_dtype dtype, int hq, int hkv, int head_dim,
                             int vocab, size_t* fwd, size_t* bwd, size_t* logprob, size_t* loss);
 
