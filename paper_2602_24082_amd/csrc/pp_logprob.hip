@@ -315,16 +315,17 @@ __global__ __launch_bounds__(kLpThreads) void logprob_bwd_kernel(LogprobBwdLaunc
 // same registers and streamed out, so each row costs one read and one write of
 // HBM (the two-pass kernel above reads it twice).  Rows that predict nothing
 // are streamed zeros.  Used when the row's 16-byte vectors fit
-// (vocab <= kLpbThreads * kLpbVecs * elements per vector: 131072 bf16 or 65536
-// fp32 values) and rows are 16-byte aligned.  1024 threads x 16 vectors holds a
-// 128256-entry bf16 row in 111 VGPRs without spilling; at 4 waves per SIMD it
+// (vocab <= kLpbThreads * kLpbVecs * elements per vector: 155648 bf16 or 77824
+// fp32 values, so a 152064-entry bf16 vocabulary fits as well as a 128256-entry
+// one) and rows are 16-byte aligned.  1024 threads x 19 vectors take 128 VGPRs
+// without spilling, the most that still allows 4 waves per SIMD; that shape
 // kept HBM busier than 512 x 40 (2 waves per SIMD, 0.73 against 0.77 ms on the
 // 8B-shaped batch) and than 768 x 27 or 1024 x 20 (both spill).
 #ifndef PP_LPB_THREADS
 #define PP_LPB_THREADS 1024
 #endif
 #ifndef PP_LPB_VECS
-#define PP_LPB_VECS 16
+#define PP_LPB_VECS 19
 #endif
 constexpr int kLpbThreads = PP_LPB_THREADS;
 constexpr int kLpbVecs = PP_LPB_VECS;

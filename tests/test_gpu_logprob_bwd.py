@@ -94,11 +94,17 @@ def test_logprob_bwd_llama_vocab_k4():
 
 
 def test_logprob_bwd_register_row_limit():
-    # fp32 rows of exactly 1024 threads x 16 vectors x 4 values (held in
+    # fp32 rows of exactly 1024 threads x 19 vectors x 4 values (held in
     # registers, read once) and one 16-byte vector longer (the two-read kernel)
     pack = wl.make_pack([6, 3], [[5, 2], [4, 1, 3]], pad=[1, 0])
-    _check_bwd(pack, 65536, torch.float32, 3.0, 185)
-    _check_bwd(pack, 65540, torch.float32, 3.0, 186)
+    _check_bwd(pack, 77824, torch.float32, 3.0, 185)
+    _check_bwd(pack, 77828, torch.float32, 3.0, 186)
+
+
+def test_logprob_bwd_qwen_vocab():
+    # a 152064-entry bf16 vocabulary (the 72B-shaped workloads): register rows
+    pack = wl.make_pack([33, 8], [[12, 1], [20, 5, 3]], pad=[0, 2])
+    _check_bwd(pack, 152064, torch.bfloat16, 3.0, 187)
 
 
 def _random_logprob_pack(rng):
