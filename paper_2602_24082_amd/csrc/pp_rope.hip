@@ -9,7 +9,7 @@
 // gradient back through the embedding).  Memory-bound: one thread owns four
 // pairs of one token, computes their cosines and sines once and applies them to
 // every head of the token, so a head's row is read and written in 16 coalesced
-// 8-byte pieces per half.
+// 8-byte pieces per half; four heads' loads are in flight at a time.
 
 #include <hip/hip_runtime.h>
 
@@ -48,9 +48,7 @@ __global__ __launch_bounds__(256) void rope_kernel(RopeLaunch a) {
   const int half = a.head_dim / 2;
   const T* x = reinterpret_cast<const T*>(a.x) + t * a.heads * a.head_dim;
   T* y = reinterpret_cast<T*>(a.y) + t * a.heads * a.head_dim;
-  for (int h = 0; h < a.heads; ++h) {
-    const V4 x1 = *reinterpret_cast<const V4*>(x + h * a.head_dim + j0);
-    const V4 x2 = *reinterpret_cast<const V4*>(x + h * a.head_dim + half + j0);
+  auto rotate = [&](const V4& x1, const V4& x2, int h) {
     f32x4 y1, y2;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -60,7 +58,25 @@ __global__ __launch_bounds__(256) void rope_kernel(RopeLaunch a) {
     }
     store4<T>(y + h * a.head_dim + j0, y1);
     store4<T>(y + h * a.head_dim + half + j0, y2);
+  };
+  // kHb heads' loads are issued before any of their stores, so each thread has
+  // 2 kHb loads in flight (x and y may be the same tensor: a head's elements are
+  // read and written by this thread only, and different heads do not overlap)
+  constexpr int kHb = 4;
+  int h = 0;
+  for (; h + kHb <= a.heads; h += kHb) {
+    V4 x1[kHb], x2[kHb];
+#pragma unroll
+    for (int i = 0; i < kHb; ++i) {
+      x1[i] = *reinterpret_cast<const V4*>(x + (h + i) * a.head_dim + j0);
+      x2[i] = *reinterpret_cast<const V4*>(x + (h + i) * a.head_dim + half + j0);
+    }
+#pragma unroll
+    for (int i = 0; i < kHb; ++i) rotate(x1[i], x2[i], h + i);
   }
+  for (; h < a.heads; ++h)
+    rotate(*reinterpret_cast<const V4*>(x + h * a.head_dim + j0),
+           *reinterpret_cast<const V4*>(x + h * a.head_dim + half + j0), h);
 }
 
 }  // namespace
