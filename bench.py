@@ -1,6 +1,6 @@
 """Benchmark of the preference-packing hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config WORKLOAD]
 
 One step = one pass of the whole hot path over one packed batch of the
 Llama-3-8B-shaped workload (8 rows, 32 query / 8 kv heads, head_dim 128, prompt
@@ -333,11 +333,10 @@ def stored_ds_leg(pack, hq, hkv, d, dev, with_kernels=True):
     return out
 
 
-def workload_leg(cfg_index, dev):
+def workload_leg(cfg, dev):
     """Attention fwd+bwd of another workload: useful TFLOP/s of the whole pass
     (HIP events around it, no per-launch events inside) and per kernel, and the
     speedup over the same kernels on the unpacked padded layout."""
-    cfg = wl.CONFIGS[cfg_index]
     pack = wl.config_pack(cfg)
     hq, hkv, d = cfg.hq, cfg.hkv, cfg.head_dim
     U = useful_pairs(pack)
@@ -361,7 +360,7 @@ def chain_sorting(dev, reps=1):
     longest pair, log-probs over the unpadded pairs).  Reports the single-GPU
     total over the 8 batches and a simulated 8-rank data-parallel step (each
     virtual rank runs 2 rows; a step costs its slowest rank)."""
-    cfg = wl.CONFIGS[4]
+    cfg = wl.DPO_CHAIN
     P, L, unsorted, sorted_b = wl.dpo_chain_pool(cfg)
     V = cfg.vocab
     max_tokens = 0
@@ -552,7 +551,8 @@ def main():
     ap.add_argument("--prewarm-s", type=float, default=2.0,
                     help="untimed steps for this many seconds before the warm-up steps: the first GPU "
                          "process on a fresh machine otherwise times some steps before the clocks settle")
-    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--config", default=wl.LLAMA3_8B.name, choices=sorted(wl.BY_NAME),
+                    help="the workload of the timed steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--calib-copy", action="store_true")
@@ -578,15 +578,14 @@ def main():
     if args.chain_sorting:
         print(json.dumps(chain_sorting(dev)))
         return
+    cfg = wl.BY_NAME[args.config]
     if args.attn_loop:
-        cfg = wl.CONFIGS[args.config]
         pack = wl.config_pack(cfg)
         ms = time_attention(pack, cfg.hq, cfg.hkv, cfg.head_dim, dev, iters=args.attn_loop, warmup=2,
                             store_ds=args.store_ds)
         print(json.dumps({"workload": cfg.name, "store_ds": args.store_ds, "attn_fwd_bwd_ms": round(ms, 4)}))
         return
 
-    cfg = wl.CONFIGS[args.config]
     pack = wl.config_pack(cfg)
     T = pack.total_tokens
     seed = wl.tensor_seed(cfg.index, 0)
@@ -686,7 +685,7 @@ def main():
 
     bound, work = per_launch[dom]
     avg_ms = kern[dom][0] / kern[dom][1]
-    traffic = traffic_from_profile(dom) if args.config == 1 else None
+    traffic = traffic_from_profile(dom) if cfg is wl.LLAMA3_8B else None
     if bound == "mfma":
         ach = work / (avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
@@ -726,7 +725,7 @@ def main():
         gbs = (n_rows * V * 2 + n_rows * 16) / (lp_ms * 1e-3) / 1e9
         logprob = {"kernel": "pp_logprob_rows", "GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
                    "rows": n_rows, "vocab": V, "avg_ms": round(lp_ms, 4),
-                   "traffic": traffic_from_profile("pp_logprob_rows") if args.config == 1 else None}
+                   "traffic": traffic_from_profile("pp_logprob_rows") if cfg is wl.LLAMA3_8B else None}
 
     # log-prob backward (the next link of the DPO chain): timed on its own, the
     # step above keeps to the forward hot path
@@ -750,7 +749,7 @@ def main():
         logprob_bwd = {"kernel": "pp_logprob_bwd", "GB_per_s": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
                        "algorithmic_bytes": nbytes, "avg_ms": round(kb_ms, 4),
                        "bytes_rule": "needed logit rows read once + every dlogits row written once (bf16)",
-                       "traffic": traffic_from_profile("pp_logprob_bwd") if args.config == 1 else None}
+                       "traffic": traffic_from_profile("pp_logprob_bwd") if cfg is wl.LLAMA3_8B else None}
     del dlogits
     # the gathered form: only the predicting rows are written
     n_g = pp.pp_logprob_row_count(pack)
@@ -817,7 +816,7 @@ def main():
         torch.cuda.empty_cache()
         memory = memory_leg(pack, hq, cfg.hkv, d, dev)
         stored = stored_ds_leg(pack, hq, cfg.hkv, d, dev)
-        workloads = {wl.CONFIGS[i].name: workload_leg(i, dev) for i in (2, 3, 4) if i != args.config}
+        workloads = {c.name: workload_leg(c, dev) for c in (wl.RM_K4, wl.LONG_PREFIX, wl.DPO_CHAIN) if c is not cfg}
         chain = chain_sorting(dev)
 
     cpu = None

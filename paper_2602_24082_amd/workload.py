@@ -123,6 +123,9 @@ CONFIGS: List[Config] = [
     Config("dpo_chain_qwen72b_gqa64x8_d128_v152064", 4, 64, 8, 128, 16, "bf16", vocab=152064,
            logit_sigma=1.0, beta=0.1, with_ref=True, capacity=8192),
 ]
+# the configurations by name (index is only their seed stream)
+TINY_FP32, LLAMA3_8B, RM_K4, LONG_PREFIX, DPO_CHAIN = CONFIGS
+BY_NAME = {c.name: c for c in CONFIGS}
 
 
 def _rng(cfg_index: int, stream: int, extra: int = 0) -> np.random.Generator:

@@ -71,7 +71,7 @@ def test_export_golden_fixture_row():
 
 def test_export_config_sized_rows():
     """Full-size rows of the 8B-shaped workload at the kernels' own tile sizes."""
-    pack = wl.config_pack(wl.CONFIGS[1], rows=2)
+    pack = wl.config_pack(wl.LLAMA3_8B, rows=2)
     for bq, bk in [(128, 64), (32, 128)]:
         _, _, tiles = binding.pp_pack_export(pack, bq, bk)
         assert (tiles == orc.pack_tile_classes(*pack.oracle_args(), bq, bk)).all()
@@ -225,8 +225,8 @@ def test_loss_argument_checks():
 
 
 def test_workspace_sizes_grow_with_batch():
-    small = wl.config_pack(wl.CONFIGS[0])
-    big = wl.config_pack(wl.CONFIGS[1])
+    small = wl.config_pack(wl.TINY_FP32)
+    big = wl.config_pack(wl.LLAMA3_8B)
     a = binding.pp_workspace_size(small, 4, 4, 64, 1000, logprob=True)
     b = binding.pp_workspace_size(big, 32, 8, 128, 128256, logprob=True)
     assert all(x > 0 for x in a) and all(y >= x for x, y in zip(a, b))

@@ -43,8 +43,7 @@ def _pick_row(pack, which):
     return int(np.argsort(n, kind="stable")[len(n) // 2])  # median length
 
 
-def _attention_sample(cfg_index, group, which, store_ds=False):
-    cfg = wl.CONFIGS[cfg_index]
+def _attention_sample(cfg, group, which, store_ds=False):
     pack = wl.config_pack(cfg)
     seed = wl.tensor_seed(cfg.index, 0)
     q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, seed, torch.bfloat16, DEV)
@@ -78,35 +77,36 @@ def _attention_sample(cfg_index, group, which, store_ds=False):
 
 @pytest.mark.parametrize("which", ["longest", "shortest"])
 def test_fullsize_llama3_8b_attention(which):
-    _attention_sample(1, group=3, which=which)
+    _attention_sample(wl.LLAMA3_8B, group=3, which=which)
 
 
 @pytest.mark.parametrize("which", ["longest", "shortest"])
 def test_fullsize_rm_k4_attention(which):
-    _attention_sample(2, group=5, which=which)
+    _attention_sample(wl.RM_K4, group=5, which=which)
 
 
 @pytest.mark.parametrize("which", ["median", "shortest"])
 def test_fullsize_long_prefix_attention(which):
-    _attention_sample(3, group=7, which=which)
+    _attention_sample(wl.LONG_PREFIX, group=7, which=which)
 
 
 @pytest.mark.parametrize("which", ["longest", "shortest"])
 def test_fullsize_dpo_chain_attention(which):
-    _attention_sample(4, group=0, which=which)
+    _attention_sample(wl.DPO_CHAIN, group=0, which=which)
 
 
-@pytest.mark.parametrize("cfg_index,group,which", [(1, 6, "longest"), (3, 2, "median"), (4, 5, "longest")])
-def test_fullsize_attention_stored_ds(cfg_index, group, which):
+@pytest.mark.parametrize("name,group,which", [("llama3_8b_gqa32x8_d128_k2", 6, "longest"),
+                                              ("long_prefix_qwen72b_gqa64x8_d128", 2, "median"),
+                                              ("dpo_chain_qwen72b_gqa64x8_d128_v152064", 5, "longest")])
+def test_fullsize_attention_stored_ds(name, group, which):
     """The stored-dS backward on whole benchmarked batches (0.45 to 12 GB of dS)."""
-    _attention_sample(cfg_index, group=group, which=which, store_ds=True)
+    _attention_sample(wl.BY_NAME[name], group=group, which=which, store_ds=True)
 
 
-def _attention_rope_sample(cfg_index, group, base):
+def _attention_rope_sample(cfg, group, base):
     """The fused rotary path on a whole benchmarked batch; the oracle recomputes
     one row and one kv-head group on the bf16-rounded rotations the kernels
     attend with, and carries the gradients back through the exact rotation."""
-    cfg = wl.CONFIGS[cfg_index]
     pack = wl.config_pack(cfg)
     seed = wl.tensor_seed(cfg.index, 0)
     q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, seed, torch.bfloat16, DEV)
@@ -142,11 +142,11 @@ def _attention_rope_sample(cfg_index, group, base):
 
 
 def test_fullsize_llama3_8b_attention_rope():
-    _attention_rope_sample(1, group=2, base=500000.0)
+    _attention_rope_sample(wl.LLAMA3_8B, group=2, base=500000.0)
 
 
 def test_fullsize_long_prefix_attention_rope():
-    _attention_rope_sample(3, group=4, base=1000000.0)
+    _attention_rope_sample(wl.LONG_PREFIX, group=4, base=1000000.0)
 
 
 def _compact_response(pack, b, k, logits, tokens):
@@ -170,8 +170,7 @@ def _compact_response(pack, b, k, logits, tokens):
     return seq[0, 0]
 
 
-def _logprob_sample(cfg_index, stream, n_samples=6):
-    cfg = wl.CONFIGS[cfg_index]
+def _logprob_sample(cfg, stream, n_samples=6):
     pack = wl.config_pack(cfg)
     seed = wl.tensor_seed(cfg.index, 0)
     T = pack.total_tokens
@@ -181,7 +180,7 @@ def _logprob_sample(cfg_index, stream, n_samples=6):
     torch.cuda.synchronize()
     seq_c = seq.double().cpu().numpy()
     tok_c = tok.double().cpu().numpy()
-    rng = np.random.default_rng(cfg_index)
+    rng = np.random.default_rng(cfg.index)
     picks = [(int(b), int(rng.integers(0, int(pack.num_resp[b])))) for b in rng.integers(0, pack.num_rows, n_samples)]
     for b, k in picks:
         want = _compact_response(pack, b, k, logits, tokens)
@@ -197,8 +196,8 @@ def _logprob_sample(cfg_index, stream, n_samples=6):
 
 
 def test_fullsize_rm_k4_logprob_and_bt_loss():
-    pack, seq = _logprob_sample(2, wl.STREAM_LOGITS_POL)
-    cfg = wl.CONFIGS[2]
+    pack, seq = _logprob_sample(wl.RM_K4, wl.STREAM_LOGITS_POL)
+    cfg = wl.RM_K4
     loss, rows, grad = pp.pp_dpo_loss(pack.num_resp.tolist(), seq, None, cfg.beta)
     want, want_rows, want_g = orc.pair_loss(pack.num_resp.tolist(), seq.double().cpu().numpy(), None, cfg.beta)
     assert abs(float(loss) - want) <= 1e-4 * abs(want)
@@ -206,9 +205,9 @@ def test_fullsize_rm_k4_logprob_and_bt_loss():
 
 
 def test_fullsize_dpo_chain_logprob_and_loss():
-    pack, s_pol = _logprob_sample(4, wl.STREAM_LOGITS_POL, n_samples=4)
-    _, s_ref = _logprob_sample(4, wl.STREAM_LOGITS_REF, n_samples=4)
-    cfg = wl.CONFIGS[4]
+    pack, s_pol = _logprob_sample(wl.DPO_CHAIN, wl.STREAM_LOGITS_POL, n_samples=4)
+    _, s_ref = _logprob_sample(wl.DPO_CHAIN, wl.STREAM_LOGITS_REF, n_samples=4)
+    cfg = wl.DPO_CHAIN
     loss, rows, grad = pp.pp_dpo_loss(pack.num_resp.tolist(), s_pol, s_ref, cfg.beta)
     want, want_rows, want_g = orc.pair_loss(pack.num_resp.tolist(), s_pol.double().cpu().numpy(),
                                             s_ref.double().cpu().numpy(), cfg.beta)

@@ -76,7 +76,7 @@ def _check_bwd(pack, V, dtype, sigma, seed, dseq=None):
 
 
 def test_logprob_bwd_tiny_fp32():
-    _check_bwd(wl.config_pack(wl.CONFIGS[0]), 1000, torch.float32, 2.0, 171)
+    _check_bwd(wl.config_pack(wl.TINY_FP32), 1000, torch.float32, 2.0, 171)
 
 
 def test_logprob_bwd_bf16_odd_vocab_and_edges():
@@ -167,7 +167,7 @@ def test_logprob_bwd_fullsize_rm_k4_sampled():
     # the reward-model batch at full size (17.7k rows x 128256, bf16); the oracle
     # recomputes sampled rows from compact packs: single-label rows of sampled
     # responses, and every row's last prompt position (all K first tokens)
-    cfg = wl.CONFIGS[2]
+    cfg = wl.RM_K4
     pack = wl.config_pack(cfg)
     T, V = pack.total_tokens, cfg.vocab
     seed = wl.tensor_seed(cfg.index, 0)

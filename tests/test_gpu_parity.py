@@ -89,7 +89,7 @@ def _check_attention(pack, hq, hkv, d, dtype, seed, check_bwd=True, inputs=None,
 @pytest.mark.parametrize("store_ds", [False, True])
 def test_tiny_fp32_config(store_ds):
     """4 rows, 4 heads (MHA), d 64, fp32 inputs, K=2 (the tiny check config)."""
-    cfg = wl.CONFIGS[0]
+    cfg = wl.TINY_FP32
     _check_attention(wl.config_pack(cfg), cfg.hq, cfg.hkv, cfg.head_dim, torch.float32, 11, store_ds=store_ds)
 
 
@@ -293,7 +293,7 @@ def test_logprob_random_sweep(seed):
 
 
 def test_logprob_tiny_fp32():
-    cfg = wl.CONFIGS[0]
+    cfg = wl.TINY_FP32
     _check_logprob(wl.config_pack(cfg), 1000, torch.float32, 2.0, 71)
 
 
@@ -344,7 +344,7 @@ def test_dpo_loss_and_bt_loss():
 
 def test_full_chain_tiny_config():
     """Tiny config end to end: policy and reference log-probs, then DPO at beta 0.1."""
-    cfg = wl.CONFIGS[0]
+    cfg = wl.TINY_FP32
     pack = wl.config_pack(cfg)
     s_pol = _check_logprob(pack, cfg.vocab, torch.float32, cfg.logit_sigma, 100)
     s_ref = _check_logprob(pack, cfg.vocab, torch.float32, cfg.logit_sigma, 200)

@@ -93,7 +93,7 @@ def test_rotary_plan_equals_rotary_entry_points():
 
 def test_planned_full_size_workload_matches_self_contained():
     """The 8B-shaped benchmark batch: planned == self-contained, bit for bit."""
-    cfg = wl.CONFIGS[1]
+    cfg = wl.LLAMA3_8B
     pack = wl.config_pack(cfg)
     print(f"case plan-fullsize {cfg.name} T={pack.total_tokens}", flush=True)
     q, k, v, do = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, 9, torch.bfloat16, DEV)

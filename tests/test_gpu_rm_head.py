@@ -62,13 +62,13 @@ def test_rm_head_fp32_edges():
 
 
 def test_rm_head_bf16_k4_full_size():
-    cfg = wl.CONFIGS[2]
+    cfg = wl.RM_K4
     _check(wl.config_pack(cfg), 4096, torch.bfloat16, 302)
 
 
 def test_rm_head_bradley_terry_chain():
     # scores -> Bradley-Terry loss over all ranked pairs -> head gradients
-    cfg = wl.CONFIGS[2]
+    cfg = wl.RM_K4
     pack = wl.config_pack(cfg)
     hidden, w, _ = _inputs(pack, 1024, torch.float32, 303)
     hg, wg = hidden.to(DEV), w.to(DEV)

@@ -120,7 +120,7 @@ def test_fused_rope_attention_matches_oracle(d, hq, hkv, store_ds):
 
 
 def test_fused_rope_attention_fp32_tiny_config():
-    cfg = wl.CONFIGS[0]
+    cfg = wl.TINY_FP32
     pack = wl.config_pack(cfg)
     _check_fused(pack, cfg.hq, cfg.hkv, cfg.head_dim, 10000.0, torch.float32, 78)
 

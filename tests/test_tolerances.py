@@ -118,7 +118,7 @@ def test_fp32_lse_slack_covers_input_rounding():
     change exceeds the plain bar on the tiny fp32 workload and stays inside the
     bar widened by fp32_lse_slack."""
     from tolerances import fp32_lse_slack, lse_excess
-    cfg = wl.CONFIGS[0]
+    cfg = wl.TINY_FP32
     pack = wl.config_pack(cfg)
     q, k, _, _ = wl.qkv(pack, cfg.hq, cfg.hkv, cfg.head_dim, 11, torch.float32, device="cpu")
     args = pack.oracle_args()

@@ -31,7 +31,7 @@ def _run(pack, hq, hkv, d, seed):
 
 
 def test_noalloc_forward_equals_workspace_forward():
-    big = wl.config_pack(wl.CONFIGS[1])  # the 8B-shaped batch, 10861 tokens
+    big = wl.config_pack(wl.LLAMA3_8B)  # the 8B-shaped batch, 10861 tokens
     _run(big, 32, 8, 128, 7)
     small = wl.make_pack([300, 0, 129, 5], [[70, 45], [33, 64], [1, 0, 200], [130]], pad=[3, 0, 0, 17])
     q, k, v, o, lse = _run(small, 8, 2, 128, 8)
