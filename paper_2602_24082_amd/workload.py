@@ -141,23 +141,23 @@ def draw_lengths(cfg: Config, rows: Optional[int] = None, batch: int = 0):
     """Prompt and response lengths of one batch of a configuration."""
     B = cfg.rows if rows is None else rows
     rng = _rng(cfg.index, 0, batch)
-    if cfg.index == 0:
+    if cfg.name == TINY_FP32.name:
         P = rng.integers(64, 128, size=B, endpoint=True)
         L = rng.integers(16, 64, size=(B, 2), endpoint=True)
-    elif cfg.index == 1:
+    elif cfg.name == LLAMA3_8B.name:
         P = rng.integers(256, 1536, size=B, endpoint=True)
         L = rng.integers(64, 512, size=(B, 2), endpoint=True)
-    elif cfg.index == 2:
+    elif cfg.name == RM_K4.name:
         P = rng.integers(512, 2048, size=B, endpoint=True)
         L = rng.integers(32, 384, size=(B, 4), endpoint=True)
-    elif cfg.index == 3:
+    elif cfg.name == LONG_PREFIX.name:
         P = rng.integers(2048, 6144, size=B, endpoint=True)
         L = rng.integers(64, 256, size=(B, 2), endpoint=True)
-    elif cfg.index == 4:
+    elif cfg.name == DPO_CHAIN.name:
         P = _lognormal_int(rng, 1024, 0.6, 1, 6144, B)
         L = _lognormal_int(rng, 192, 0.6, 1, 1024, B * 2).reshape(B, 2)
     else:
-        raise ValueError(cfg.index)
+        raise ValueError(cfg.name)
     return P.tolist(), L.tolist()
 
 
