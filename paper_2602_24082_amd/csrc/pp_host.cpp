@@ -129,20 +129,6 @@ inline int64_t overlap(int64_t a0, int64_t a1, int64_t b0, int64_t b1) {
   return hi > lo ? hi - lo : 0;
 }
 
-// Row-relative start of the segment holding token t (0 for the prompt), or -1
-// for padding.
-inline int32_t seg_start(const Row& r, int32_t t) {
-  if (t < r.P) return 0;
-  if (t >= r.valid) return -1;
-  // responses are contiguous from P, so the last offset <= t wins
-  int32_t lo = r.P;
-  for (int k = 0; k < r.K; ++k) {
-    if (r.off[k] <= t && t < r.off[k] + r.len[k]) return r.off[k];
-    if (r.off[k] <= t) lo = r.off[k];
-  }
-  return lo;
-}
-
 // Segment id: 0 prompt, k+1 response k, -1 padding.
 inline int32_t seg_id(const Row& r, int32_t t) {
   if (t < r.P) return 0;
@@ -290,10 +276,17 @@ void build_kplan(const Batch& bt, int BN, std::vector<KTileItem>* out) {
   });
 }
 
+// The per-token arrays below are filled segment by segment: a validated row is
+// its prompt [0, P), then its responses back to back from P, then padding.
+// seg_lo: row-relative start of the token's segment (0 in the prompt, o_k in
+// response k, -1 for padding).
 void build_seg_lo(const Batch& bt, std::vector<int32_t>* out) {
   out->assign(bt.sumT, -1);
-  for (const Row& r : bt.rows)
-    for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_start(r, t);
+  int32_t* o = out->data();
+  for (const Row& r : bt.rows) {
+    std::fill(o + r.tok0, o + r.tok0 + r.P, 0);
+    for (int k = 0; k < r.K; ++k) std::fill(o + r.tok0 + r.off[k], o + r.tok0 + r.off[k] + r.len[k], r.off[k]);
+  }
 }
 
 // One past the last query that can see key t (row-relative): a prompt key is
@@ -306,10 +299,15 @@ inline int32_t seg_end(const Row& r, int32_t t) {
   return 0;
 }
 
+// seg_hi: seg_end of every token.
 void build_seg_hi(const Batch& bt, std::vector<int32_t>* out) {
   out->assign(bt.sumT, 0);
-  for (const Row& r : bt.rows)
-    for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = seg_end(r, t);
+  int32_t* o = out->data();
+  for (const Row& r : bt.rows) {
+    std::fill(o + r.tok0, o + r.tok0 + r.P, r.valid);
+    for (int k = 0; k < r.K; ++k)
+      std::fill(o + r.tok0 + r.off[k], o + r.tok0 + r.off[k] + r.len[k], r.off[k] + r.len[k]);
+  }
 }
 
 // Panels of the stored dS: per row, per 32-key block KB, the query blocks
@@ -354,10 +352,15 @@ int32_t token_position(const Row& r, int32_t t) {
   return 0;
 }
 
+// Positions: token_position of every token.
 void build_positions(const Batch& bt, std::vector<int32_t>* out) {
   out->assign(bt.sumT, 0);
-  for (const Row& r : bt.rows)
-    for (int32_t t = 0; t < r.T; ++t) (*out)[r.tok0 + t] = token_position(r, t);
+  int32_t* o = out->data();
+  for (const Row& r : bt.rows) {
+    for (int32_t t = 0; t < r.P; ++t) o[r.tok0 + t] = t;
+    for (int k = 0; k < r.K; ++k)
+      for (int32_t j = 0; j < r.len[k]; ++j) o[r.tok0 + r.off[k] + j] = r.P + j;
+  }
 }
 
 // Rotary frequencies base^(-2j/d), j < d/2, in fp64.
