@@ -158,6 +158,23 @@ class _DescHolder:
         return ctypes.byref(self.desc)
 
 
+def _desc_of(pack: Pack) -> _DescHolder:
+    """The C descriptor of a pack, built on first use and kept on the pack (a
+    pack is usually passed to many calls: every layer's attention, the
+    log-probs, the loss); rebuilt whenever the pack's arrays have changed."""
+    key = (pack.num_rows, pack.max_resp) + tuple(
+        np.asarray(a).tobytes() for a in (pack.row_start, pack.prompt_len, pack.num_resp, pack.resp_off, pack.resp_len))
+    h = getattr(pack, "_pp_desc", None)
+    if h is None or h.key != key:
+        h = _DescHolder(pack)
+        h.key = key
+        try:
+            pack._pp_desc = h
+        except AttributeError:  # a pack type that takes no new attributes: no caching
+            pass
+    return h
+
+
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.bfloat16:
         return PP_BF16
@@ -186,7 +203,7 @@ def pp_workspace_size(pack: Pack, hq: int = 1, hkv: int = 1, head_dim: int = 64,
                       fwd=True, bwd=True, logprob=False, loss=True, dtype: int = PP_BF16):
     """Workspace bytes (fwd, bwd, logprob, loss); entries not asked for are None.
     dtype is the attention input dtype code (PP_BF16 or PP_FP32)."""
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     vals = [ctypes.c_size_t(0) for _ in range(4)]
     want = [fwd, bwd, logprob, loss]
     args = [ctypes.byref(v) if w else None for v, w in zip(vals, want)]
@@ -196,7 +213,7 @@ def pp_workspace_size(pack: Pack, hq: int = 1, hkv: int = 1, head_dim: int = 64,
 
 def pp_bwd_stored_ds_workspace_size(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16):
     """(bwd, plan) workspace bytes that select the backward's stored-dS mode."""
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     b, p = ctypes.c_size_t(0), ctypes.c_size_t(0)
     _check(lib().pp_bwd_stored_ds_workspace_size(h.ref, dtype, hq, hkv, head_dim, ctypes.byref(b), ctypes.byref(p)))
     return int(b.value), int(p.value)
@@ -214,7 +231,7 @@ def pp_attn_fwd(pack: Pack, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, s
     """Packed attention forward; returns (o [sumT,hq,d], lse [hq,sumT] fp32)."""
     T, hq, d = q.shape
     hkv = k.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
@@ -234,7 +251,7 @@ def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, 
     holds the stored dS when store_ds is set (else the dQ pass recomputes)."""
     T, hq, d = q.shape
     hkv = k.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
@@ -247,7 +264,7 @@ def pp_attn_bwd(pack: Pack, q, k, v, o, lse, dout, scale: float = 0.0, dq=None, 
 
 
 def pp_rope_workspace_size(pack: Pack, head_dim: int) -> int:
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     n = ctypes.c_size_t(0)
     _check(lib().pp_rope_workspace_size(h.ref, head_dim, ctypes.byref(n)))
     return n.value
@@ -256,7 +273,7 @@ def pp_rope_workspace_size(pack: Pack, head_dim: int) -> int:
 def pp_rope(pack: Pack, x: torch.Tensor, rope_base: float, inverse: bool = False, out=None, ws=None):
     """Rotary embedding of x [sumT, heads, d] on the packed position IDs; out may be x."""
     T, H, d = x.shape
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     out = torch.empty_like(x) if out is None else out
     if ws is None:
         ws = _workspace(pp_rope_workspace_size(pack, d), x.device)
@@ -272,7 +289,7 @@ def pp_attn_fwd_noalloc(pack: Pack, q: torch.Tensor, k: torch.Tensor, v: torch.T
     when they are not given."""
     T, hq, d = q.shape
     hkv = k.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
@@ -288,7 +305,7 @@ def pp_attn_fwd_rope(pack: Pack, q, k, v, rope_base: float, scale: float = 0.0, 
     (o, lse, q_rot or None, k_rot)."""
     T, hq, d = q.shape
     hkv = k.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     out = torch.empty_like(q) if out is None else out
     if lse is None:
         lse = torch.empty(hq, T, dtype=torch.float32, device=q.device)
@@ -310,7 +327,7 @@ def pp_attn_bwd_rope(pack: Pack, q_rot, k_rot, v, o, lse, dout, rope_base: float
     (workspace and mode as pp_attn_bwd)."""
     T, hq, d = q_rot.shape
     hkv = k_rot.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dq = torch.empty_like(q_rot) if dq is None else dq
     dk = torch.empty_like(k_rot) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
@@ -338,7 +355,7 @@ class PlanHandle:
 
 
 def pp_plan_workspace_size(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP_BF16) -> int:
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     n = ctypes.c_size_t(0)
     _check(lib().pp_plan_workspace_size(h.ref, dtype, hq, hkv, head_dim, ctypes.byref(n)))
     return n.value
@@ -349,7 +366,7 @@ def pp_plan_create(pack: Pack, hq: int, hkv: int, head_dim: int, dtype: int = PP
                    device="cuda:0", store_ds: bool = False) -> PlanHandle:
     """Plans the pack once and stages the metadata into ws on the current stream
     (a workspace allocated here holds the stored dS when store_ds is set)."""
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     if ws is None:
         nb = (pp_bwd_stored_ds_workspace_size(pack, hq, hkv, head_dim, dtype)[1] if store_ds
               else pp_plan_workspace_size(pack, hq, hkv, head_dim, dtype))
@@ -395,7 +412,7 @@ def pp_seq_logprob(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, want_
                    seq=None, tok=None, ws=None):
     """Per-response summed log-probs [B, K_max] (and per-token [sumT] if asked)."""
     V = logits.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dev = logits.device
     if seq is None:
         seq = torch.empty(pack.num_rows, max(pack.max_resp, 1), dtype=torch.float32, device=dev)
@@ -415,7 +432,7 @@ def pp_seq_logprob_bwd(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, d
                        dlogits=None, ws=None):
     """Gradient of sum(dseq * seq_logp) w.r.t. the logits: [sumT, V] in the logits' dtype."""
     V = logits.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dev = logits.device
     if dlogits is None:
         dlogits = torch.empty_like(logits)
@@ -433,7 +450,7 @@ def pp_seq_logprob_bwd(pack: Pack, logits: torch.Tensor, tokens: torch.Tensor, d
 
 def pp_logprob_row_count(pack: Pack) -> int:
     """Number of logit rows that predict a response token."""
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     n = ctypes.c_int64(0)
     _check(lib().pp_logprob_row_count(h.ref, ctypes.byref(n)))
     return int(n.value)
@@ -444,7 +461,7 @@ def pp_seq_logprob_bwd_rows(pack: Pack, logits: torch.Tensor, tokens: torch.Tens
     """Gradient of sum(dseq * seq_logp) on the predicting logit rows only:
     (dlogits_rows [n, V] in the logits' dtype, row_index [n] int32)."""
     V = logits.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dev = logits.device
     n = pp_logprob_row_count(pack)
     if dlogits_rows is None:
@@ -464,7 +481,7 @@ def pp_seq_logprob_bwd_rows(pack: Pack, logits: torch.Tensor, tokens: torch.Tens
 
 
 def pp_rm_workspace_size(pack: Pack) -> int:
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     n = ctypes.c_size_t(0)
     _check(lib().pp_rm_workspace_size(h.ref, ctypes.byref(n)))
     return n.value
@@ -475,7 +492,7 @@ def pp_rm_scores(pack: Pack, hidden: torch.Tensor, w: torch.Tensor, bias: float 
     H = hidden.shape[1]
     if w.dtype != hidden.dtype or w.numel() != H:
         raise TypeError("w must be [hidden_dim] in the dtype of hidden")
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dev = hidden.device
     if scores is None:
         scores = torch.empty(pack.num_rows, max(pack.max_resp, 1), dtype=torch.float32, device=dev)
@@ -489,7 +506,7 @@ def pp_rm_scores(pack: Pack, hidden: torch.Tensor, w: torch.Tensor, bias: float 
 def pp_rm_scores_bwd(pack: Pack, hidden: torch.Tensor, w: torch.Tensor, dscores: torch.Tensor, ws=None):
     """(dhidden [sumT, H] in hidden's dtype, dw [H] float32, dbias [1] float32)."""
     H = hidden.shape[1]
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     dev = hidden.device
     if dscores.dtype != torch.float32 or not dscores.is_contiguous():
         raise TypeError("dscores must be contiguous float32 [B, K_max]")
@@ -522,7 +539,7 @@ def pp_dpo_loss(num_resp, logp_pol: torch.Tensor, logp_ref: Optional[torch.Tenso
 
 def pp_pack_stats(pack: Pack) -> dict:
     """Host-only packed-versus-unpacked accounting (tokens, pairs, Eq. (1) ratios)."""
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     out = PackStats()
     _check(lib().pp_pack_stats(h.ref, ctypes.byref(out)))
     return {name: getattr(out, name) for name, _ in PackStats._fields_}
@@ -530,7 +547,7 @@ def pp_pack_stats(pack: Pack) -> dict:
 
 def pp_pack_export(pack: Pack, block_q: int = 128, block_k: int = 64, tiles: bool = True):
     """Host-only integer export: (position_ids, segment_ids, tile_class) numpy arrays."""
-    h = _DescHolder(pack)
+    h = _desc_of(pack)
     T = max(0, pack.total_tokens)  # a broken descriptor is the library's to report
     pos = np.zeros(T, np.int32)
     seg = np.zeros(T, np.int32)
